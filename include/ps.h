@@ -1,0 +1,245 @@
+/*
+ * ps.h — C ABI of the MI355X (gfx950) prefill / decode hot path of a dense
+ * GQA decoder layer over a paged KV cache.
+ *
+ * What the calls compute. The paper's serving phases (§II-B "LLM Serving
+ * Phases and Their Metrics") are prefill — attention over every prompt token
+ * at once, compute-bound — and decode — one token per sequence per step,
+ * bound by reading the KV cache — with reasoning adding a long "think"
+ * decode before the visible answer. §III-B's roofline argument and App. B.2
+ * (eqs. flops-layer, bytes-layer) count the work of one layer of such a
+ * model. The layer is the Llama-family pre-norm layer of the models served
+ * in the evaluation:
+ *
+ *   xn = RMSNorm(x) * g_attn;  q,k,v = xn W_qkv^T;  q,k = RoPE(q,k, pos)
+ *   o  = causal GQA softmax attention of q over the sequence's keys 0..pos
+ *   h  = x + o W_o^T;  hn = RMSNorm(h) * g_ffn
+ *   out = h + (silu(hn W_g^T) * (hn W_u^T)) W_d^T
+ *
+ * RoPE is rotate-half (pairs j, j+hd/2; angle pos * theta^(-2j/hd)); query
+ * head h reads KV head h / (n_q/n_kv); attention scale 1/sqrt(hd); RMSNorm
+ * puts eps inside the square root.
+ *
+ * The per-stage KV reservation of §IV-A (each request's KV "chunk size" in
+ * tokens, CS_i) is ps_kv_alloc; the prefill / think / answer request model
+ * (§IV-A PTA disaggregation) is the ps_phase tag of ps_decode_step.
+ *
+ * Conventions for every entry point:
+ *  - Device buffers are caller-owned (e.g. torch tensors). The library never
+ *    allocates device memory; it owns only host-side metadata and a small
+ *    pinned host staging ring used to upload per-call metadata. Weight
+ *    pointers are borrowed for the duration of the call.
+ *  - Work is enqueued asynchronously on the caller's stream (a hipStream_t
+ *    passed as void*; NULL = the null stream). Nothing synchronises
+ *    implicitly, except that reuse of a staging slot waits for the copy that
+ *    last used it.
+ *  - Every function returns ps_status. Arguments, shapes and KV capacity are
+ *    validated on the host before anything is enqueued; on any error no work
+ *    is enqueued and KV metadata is unchanged. ps_last_error() returns a
+ *    thread-local message for the last failing call on this thread.
+ *  - A handle is not thread-safe; distinct handles are independent.
+ *  - Matrices are row-major. Linear weights use the W[out, in] convention
+ *    (y = x W^T). bf16 buffers hold IEEE bfloat16 bit patterns.
+ */
+#ifndef PS_H
+#define PS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ps_status;
+#define PS_OK 0
+#define PS_E_INVALID 1     /* bad argument, shape, handle, sequence or layer    */
+#define PS_E_NO_PAGES 2    /* KV pool has too few free pages for a reservation   */
+#define PS_E_CAPACITY 3    /* write beyond a sequence's reserved capacity, or a
+                              sequence would exceed max_pages_per_seq            */
+#define PS_E_HIP 4         /* a HIP runtime call or launch failed                 */
+#define PS_E_UNSUPPORTED 5 /* valid request this build does not implement         */
+
+#define PS_PAGE_TOKENS 16  /* tokens per KV page                                  */
+#define PS_GATE_UP_BLOCK 32 /* row-interleave granularity of w_gate_up            */
+
+typedef enum { PS_F32 = 0, PS_BF16 = 1 } ps_dtype;
+
+/* Request phase (§IV-A): prefill, reasoning "think" decode, answer decode.
+ * The phase may change scheduling (split-K granularity) but never the
+ * definition of the result. */
+typedef enum { PS_PHASE_PREFILL = 0, PS_PHASE_THINK = 1, PS_PHASE_ANSWER = 2 } ps_phase;
+
+typedef struct {
+  int32_t hidden;      /* d                                  */
+  int32_t n_q_heads;   /* n_q                                */
+  int32_t n_kv_heads;  /* n_kv, divides n_q                  */
+  int32_t head_dim;    /* hd: 64 or 128                      */
+  int32_t ffn;         /* F, SwiGLU width                    */
+  float rms_eps;
+  double rope_theta;
+  int32_t dtype;       /* ps_dtype of weights, activations and KV */
+} ps_layer_cfg;
+
+/* One layer's device weights, all in cfg.dtype:
+ *   attn_norm, ffn_norm  [d]
+ *   w_qkv      [d_q + 2 d_kv, d]  rows: Wq (head-major), then Wk, then Wv
+ *   w_o        [d, d_q]
+ *   w_gate_up  [2F, d]  Wg and Wu rows interleaved in blocks of
+ *              PS_GATE_UP_BLOCK (= 32) rows: block 2i = Wg rows
+ *              [32i, 32i+32), block 2i+1 = Wu rows [32i, 32i+32)
+ *              (see ps_pack_gate_up)
+ *   w_down     [d, F]                                                    */
+typedef struct {
+  const void *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate_up, *w_down;
+} ps_layer_w;
+
+typedef struct ps_kv ps_kv;
+typedef struct ps_layer ps_layer;
+
+const char* ps_last_error(void);
+const char* ps_version(void);
+
+/* Host helper: interleave Wg [F, d] and Wu [F, d] (host memory, elt_bytes
+ * per element) into the w_gate_up row order above; out has 2F*d elements.
+ * Pure layout, no arithmetic. F must be a multiple of PS_GATE_UP_BLOCK. */
+ps_status ps_pack_gate_up(const void* wg, const void* wu, int32_t F, int32_t d, int32_t elt_bytes,
+                          void* out);
+
+/* ------------------------------------------------------------------ KV pool
+ * Device layout of the caller-provided pool (cfg.dtype elements):
+ *   [n_layers][n_pages][n_kv][ K: 16 tokens x hd | V^T: hd x 16 tokens ]
+ * i.e. per (layer, page, kv head) a 16 x hd block of keys, token-major, then
+ * the same 16 tokens' values stored dimension-major. Token t of a sequence
+ * lives in page block_table[t / 16] at slot t % 16. The block table is the
+ * same for every layer. Pages are handed out from a free list whose initial
+ * order is a seeded permutation (seed 0 = identity order), so logical and
+ * physical order differ; results never depend on placement.
+ */
+size_t ps_kv_pool_bytes(const ps_layer_cfg* cfg, int32_t n_layers, int32_t n_pages);
+
+/* Host-only: creates the metadata. `pool` is borrowed until destroy and not
+ * touched by this call. */
+ps_status ps_kv_create(const ps_layer_cfg* cfg, int32_t n_layers, int32_t n_pages, int32_t max_seqs,
+                       int32_t max_pages_per_seq, void* pool, uint64_t page_order_seed, ps_kv** out);
+ps_status ps_kv_destroy(ps_kv* kv);
+
+/* Host-only metadata calls. */
+ps_status ps_kv_seq_open(ps_kv* kv, int32_t* seq);                 /* new empty sequence id        */
+ps_status ps_kv_alloc(ps_kv* kv, int32_t seq, int32_t n_tokens);   /* reserve: capacity >= len + n */
+ps_status ps_kv_commit(ps_kv* kv, int32_t n_seqs, const int32_t* seqs, const int32_t* n_tok);
+                                                                   /* len += n (once per model step,
+                                                                      after every layer wrote)    */
+ps_status ps_kv_truncate(ps_kv* kv, int32_t seq, int32_t new_len); /* len = new_len <= len; keeps
+                                                                      the reservation             */
+ps_status ps_kv_free(ps_kv* kv, int32_t seq);                      /* return pages, close seq      */
+ps_status ps_kv_seq_len(const ps_kv* kv, int32_t seq, int32_t* len);
+ps_status ps_kv_capacity(const ps_kv* kv, int32_t seq, int32_t* tokens);
+ps_status ps_kv_free_pages(const ps_kv* kv, int32_t* n);
+ps_status ps_kv_block_table(const ps_kv* kv, int32_t seq, int32_t* pages, int32_t cap, int32_t* n);
+
+/* Device calls. `ws` is caller-provided device workspace of ws_bytes bytes
+ * (at least ps_workspace_bytes for the call's size).
+ *
+ * ps_kv_append: write caller K and V rows (already rotated keys) for `layer`
+ * at positions [len, len + n_tok[i]) of each sequence; k, v are
+ * [sum n_tok, n_kv, hd] device arrays, rows grouped by sequence in order.
+ * Does not change len (see ps_kv_commit).
+ * ps_kv_gather: copy positions [0, len) of one sequence and layer into
+ * contiguous k_out, v_out [len, n_kv, hd] (export, tests). */
+ps_status ps_kv_append(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                       const int32_t* n_tok, const void* k, const void* v, void* ws, size_t ws_bytes,
+                       void* stream);
+ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k_out, void* v_out, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------ layer */
+ps_status ps_layer_create(const ps_layer_cfg* cfg, ps_layer** out);
+ps_status ps_layer_destroy(ps_layer* layer);
+
+/* Upper bound on workspace bytes for any layer call with at most max_rows
+ * new rows, max_seqs sequences and max_pages_per_seq pages per sequence. */
+size_t ps_workspace_bytes(const ps_layer_cfg* cfg, int32_t max_rows, int32_t max_seqs,
+                          int32_t max_pages_per_seq);
+
+/* Prefill (or a chunk of one): each sequence i contributes n_tok[i] rows of
+ * x_in [sum n_tok, d] at positions [len_i, len_i + n_tok[i]); its K/V for
+ * `layer` are written there (capacity must be reserved) and every row
+ * attends causally over positions 0..pos (cached prefix included). x_out
+ * [sum n_tok, d]. len is unchanged (call ps_kv_commit). */
+ps_status ps_prefill(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_seqs,
+                     const int32_t* seqs, const int32_t* n_tok, const void* x_in, void* x_out, void* ws,
+                     size_t ws_bytes, void* stream);
+
+/* Decode: one new row per sequence at position len (its K/V appended before
+ * attention, so it attends over len + 1 keys). x_in, x_out [n_seqs, d]. */
+ps_status ps_decode_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase,
+                         int32_t n_seqs, const int32_t* seqs, const void* x_in, void* x_out, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* Mixed step (chunked prefill fused with decode): the GEMMs run once over
+ * the concatenated rows — first the chunk rows of n_chunk sequences
+ * (chunk_tok[i] rows each), then one row for each of n_dec decoding
+ * sequences; attention uses the prefill path for chunk rows and the split-K
+ * decode path for decode rows. Same result as separate ps_prefill and
+ * ps_decode_step calls up to rounding. */
+ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_chunk,
+                        const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec,
+                        const int32_t* dec_seqs, const void* x_in, void* x_out, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------- single ops
+ * Stage entry points (tests, microbenchmarks). Same ownership and error
+ * rules. dtype arguments are ps_dtype; PS_F32 for fp32 buffers. */
+
+/* y[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * g; fp32 arithmetic. */
+ps_status ps_op_rmsnorm(int32_t x_dtype, int32_t g_dtype, int32_t y_dtype, int32_t rows, int32_t d,
+                        const void* x, const void* g, float eps, void* y, void* stream);
+
+/* C = epilogue(A W^T): A [M, K], W [N, K], both `dtype` (bf16 uses the MFMA
+ * path, fp32 a vector path), fp32 accumulation.
+ *   PS_EPI_STORE     C[M, N] (c_dtype)
+ *   PS_EPI_RESIDUAL  C[M, N] = R + A W^T, R of r_dtype (R may alias C when
+ *                    the dtypes match)
+ *   PS_EPI_SWIGLU    W is a w_gate_up-interleaved [N, K]; C[M, N/2] =
+ *                    silu(gate) * up with gate/up the de-interleaved halves
+ * Decode-sized M (<= 64) splits K across workgroups and needs ws of at least
+ * ps_op_gemm_workspace_bytes for its fp32 partials (0 bytes otherwise).
+ * Supported: bf16 with K % 64 == 0 and N % 256 == 0 (or M <= 64,
+ * N % 64 == 0, K % 256 == 0); fp32 any shape; SwiGLU needs N % 64 == 0. */
+#define PS_EPI_STORE 0
+#define PS_EPI_RESIDUAL 1
+#define PS_EPI_SWIGLU 2
+size_t ps_op_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K);
+ps_status ps_op_gemm(int32_t dtype, int32_t r_dtype, int32_t c_dtype, int32_t epilogue, int32_t M, int32_t N,
+                     int32_t K, const void* A, const void* W, const void* R, void* C, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* RoPE + paged KV write for `layer`: qkv [rows, d_q + 2 d_kv] (cfg.dtype)
+ * holds the QKV projection of rows grouped by sequence as in ps_prefill;
+ * writes rotated q to q_out [rows, d_q] and rotated k and v into the pages
+ * at positions [len, len + n_tok). */
+ps_status ps_op_rope_kvwrite(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                             const int32_t* n_tok, const void* qkv, void* q_out, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/* Causal attention of q [rows, n_q, hd] (rows grouped by sequence as in
+ * ps_prefill, at positions [len, len + n_tok)) over the sequence's cached
+ * keys 0..pos in the pages (the rows' own K/V must already be written).
+ * o [rows, n_q * hd]. Uses the prefill kernel. */
+ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                          const int32_t* n_tok, const void* q, void* o, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Split-K decode attention: one query row per sequence at position len
+ * (the row's own K/V already written there, not yet committed), attending
+ * over keys 0..len. q [n_seqs, n_q, hd], o [n_seqs, n_q * hd].
+ * split_pages = pages per split (0 = library choice). */
+ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                 const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
+                                 void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PS_H */

@@ -1,0 +1,804 @@
+// C ABI of libps: validation, the error model, per-call metadata upload and
+// the layer executor that sequences the kernels of one prefill, decode or
+// mixed step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/ps.h"
+#include "common.h"
+#include "kv_pool.h"
+#include "launch.h"
+
+using namespace ps;
+
+// ------------------------------------------------------------------ errors
+namespace {
+thread_local std::string g_err;
+
+ps_status fail(ps_status code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define PS_TRY try {
+#define PS_CATCH                                                   \
+  }                                                                \
+  catch (const std::bad_alloc&) {                                  \
+    return fail(PS_E_INVALID, "host allocation failed");           \
+  }                                                                \
+  catch (...) {                                                    \
+    return fail(PS_E_INVALID, "internal error");                   \
+  }
+
+ps_status hip_fail(hipError_t e, const char* what) {
+  return fail(PS_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int elt_bytes(int dt) { return dt == PS_BF16 ? 2 : 4; }
+
+ps_status check_cfg(const ps_layer_cfg* c) {
+  if (!c) return fail(PS_E_INVALID, "null config");
+  if (c->dtype != PS_F32 && c->dtype != PS_BF16) return fail(PS_E_INVALID, "dtype must be PS_F32 or PS_BF16");
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 || c->ffn <= 0)
+    return fail(PS_E_INVALID, "non-positive dimension");
+  if (c->n_q_heads % c->n_kv_heads) return fail(PS_E_INVALID, "n_kv_heads must divide n_q_heads");
+  if (c->head_dim % 2 || c->head_dim > 128) return fail(PS_E_UNSUPPORTED, "head_dim must be even and <= 128");
+  if (c->ffn % PS_GATE_UP_BLOCK) return fail(PS_E_UNSUPPORTED, "ffn must be a multiple of PS_GATE_UP_BLOCK");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.0)) return fail(PS_E_INVALID, "bad eps or rope_theta");
+  return PS_OK;
+}
+
+// Pinned host staging ring for per-call metadata. A slot is reused only
+// after the copy that last read it has completed.
+struct Staging {
+  static constexpr int kSlots = 4;
+  void* host[kSlots] = {};
+  size_t cap[kSlots] = {};
+  hipEvent_t ev[kSlots] = {};
+  bool pending[kSlots] = {};
+  int next = 0;
+
+  ~Staging() {
+    for (int s = 0; s < kSlots; ++s) {
+      if (pending[s]) (void)hipEventSynchronize(ev[s]);
+      if (ev[s]) (void)hipEventDestroy(ev[s]);
+      if (host[s]) (void)hipHostFree(host[s]);
+    }
+  }
+  // Returns the slot index or -1 (g_err set).
+  int acquire(size_t bytes, void** out) {
+    const int s = next;
+    next = (next + 1) % kSlots;
+    hipError_t e;
+    if (pending[s]) {
+      if ((e = hipEventSynchronize(ev[s])) != hipSuccess) return (hip_fail(e, "staging wait"), -1);
+      pending[s] = false;
+    }
+    if (!ev[s] && (e = hipEventCreateWithFlags(&ev[s], hipEventDisableTiming)) != hipSuccess)
+      return (hip_fail(e, "staging event"), -1);
+    if (cap[s] < bytes) {
+      if (host[s]) (void)hipHostFree(host[s]);
+      host[s] = nullptr;
+      cap[s] = 0;
+      const size_t nb = align_up(std::max<size_t>(bytes, 1 << 16), 1 << 16);
+      if ((e = hipHostMalloc(&host[s], nb, hipHostMallocDefault)) != hipSuccess)
+        return (hip_fail(e, "staging hipHostMalloc"), -1);
+      cap[s] = nb;
+    }
+    *out = host[s];
+    return s;
+  }
+  ps_status submit(int s, void* dev, size_t bytes, hipStream_t st) {
+    hipError_t e = hipMemcpyAsync(dev, host[s], bytes, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return hip_fail(e, "metadata upload");
+    if ((e = hipEventRecord(ev[s], st)) != hipSuccess) return hip_fail(e, "staging event record");
+    pending[s] = true;
+    return PS_OK;
+  }
+};
+
+// Per-call metadata, assembled on the host and uploaded in one copy to the
+// head of the caller's workspace.
+struct Meta {
+  std::vector<uint8_t> buf;
+  size_t add(const void* p, size_t bytes) {
+    size_t off = align_up(buf.size(), 256);
+    buf.resize(off + bytes);
+    if (bytes) std::memcpy(buf.data() + off, p, bytes);
+    return off;
+  }
+  size_t size() const { return align_up(buf.size(), 256); }
+};
+}  // namespace
+
+struct ps_kv {
+  ps_layer_cfg cfg;
+  int32_t n_layers;
+  void* pool;
+  size_t layer_elts;  // elements per layer
+  KvPool meta;
+  Staging staging;
+  ps_kv(const ps_layer_cfg& c, int32_t nl, int32_t np, int32_t ms, int32_t mp, void* p, uint64_t seed)
+      : cfg(c), n_layers(nl), pool(p),
+        layer_elts((size_t)np * c.n_kv_heads * 2 * PS_PAGE_TOKENS * c.head_dim), meta(np, ms, mp, seed) {}
+  void* layer_base(int layer) const {
+    return (char*)pool + (size_t)layer * layer_elts * elt_bytes(cfg.dtype);
+  }
+};
+
+struct ps_layer {
+  ps_layer_cfg cfg;
+};
+
+// ------------------------------------------------------------------ misc
+extern "C" const char* ps_last_error(void) { return g_err.c_str(); }
+extern "C" const char* ps_version(void) { return "libps 0.1.0 gfx950"; }
+
+extern "C" ps_status ps_pack_gate_up(const void* wg, const void* wu, int32_t F, int32_t d, int32_t eb, void* out) {
+  PS_TRY
+  if (!wg || !wu || !out || F <= 0 || d <= 0 || (eb != 2 && eb != 4)) return fail(PS_E_INVALID, "bad arguments");
+  if (F % PS_GATE_UP_BLOCK) return fail(PS_E_INVALID, "F must be a multiple of PS_GATE_UP_BLOCK");
+  const size_t row = (size_t)d * eb;
+  for (int32_t blk = 0; blk < F / PS_GATE_UP_BLOCK; ++blk)
+    for (int32_t r = 0; r < PS_GATE_UP_BLOCK; ++r) {
+      const size_t src = (size_t)(blk * PS_GATE_UP_BLOCK + r) * row;
+      std::memcpy((char*)out + (size_t)(2 * blk * PS_GATE_UP_BLOCK + r) * row, (const char*)wg + src, row);
+      std::memcpy((char*)out + (size_t)((2 * blk + 1) * PS_GATE_UP_BLOCK + r) * row, (const char*)wu + src, row);
+    }
+  return PS_OK;
+  PS_CATCH
+}
+
+// ------------------------------------------------------------------ KV pool
+extern "C" size_t ps_kv_pool_bytes(const ps_layer_cfg* c, int32_t n_layers, int32_t n_pages) {
+  if (!c || n_layers <= 0 || n_pages <= 0) return 0;
+  return (size_t)n_layers * n_pages * c->n_kv_heads * 2 * PS_PAGE_TOKENS * c->head_dim * elt_bytes(c->dtype);
+}
+
+extern "C" ps_status ps_kv_create(const ps_layer_cfg* c, int32_t n_layers, int32_t n_pages, int32_t max_seqs,
+                                  int32_t max_pages_per_seq, void* pool, uint64_t seed, ps_kv** out) {
+  PS_TRY
+  if (ps_status rc = check_cfg(c)) return rc;
+  if (!out) return fail(PS_E_INVALID, "null out");
+  if (n_layers <= 0 || n_pages <= 0 || max_seqs <= 0 || max_pages_per_seq <= 0)
+    return fail(PS_E_INVALID, "non-positive pool size");
+  if (!pool) return fail(PS_E_INVALID, "null pool");
+  *out = new ps_kv(*c, n_layers, n_pages, max_seqs, max_pages_per_seq, pool, seed);
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" ps_status ps_kv_destroy(ps_kv* kv) {
+  PS_TRY
+  delete kv;
+  return PS_OK;
+  PS_CATCH
+}
+
+#define CHECK_KV(kv) \
+  if (!(kv)) return fail(PS_E_INVALID, "null kv handle");
+
+extern "C" ps_status ps_kv_seq_open(ps_kv* kv, int32_t* seq) {
+  PS_TRY CHECK_KV(kv);
+  if (!seq) return fail(PS_E_INVALID, "null seq");
+  std::string e;
+  if (int rc = kv->meta.open(seq, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_alloc(ps_kv* kv, int32_t seq, int32_t n) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (int rc = kv->meta.reserve(seq, n, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_commit(ps_kv* kv, int32_t n, const int32_t* seqs, const int32_t* n_tok) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (int rc = kv->meta.commit(n, seqs, n_tok, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_truncate(ps_kv* kv, int32_t seq, int32_t new_len) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (int rc = kv->meta.truncate(seq, new_len, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_free(ps_kv* kv, int32_t seq) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (int rc = kv->meta.release(seq, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_seq_len(const ps_kv* kv, int32_t seq, int32_t* len) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (!len) return fail(PS_E_INVALID, "null len");
+  if (int rc = kv->meta.check_open(seq, e)) return fail(rc, e);
+  *len = kv->meta.seq(seq).len;
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_capacity(const ps_kv* kv, int32_t seq, int32_t* tokens) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (!tokens) return fail(PS_E_INVALID, "null tokens");
+  if (int rc = kv->meta.check_open(seq, e)) return fail(rc, e);
+  *tokens = kv->meta.capacity(seq);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_free_pages(const ps_kv* kv, int32_t* n) {
+  PS_TRY CHECK_KV(kv);
+  if (!n) return fail(PS_E_INVALID, "null n");
+  *n = kv->meta.free_pages();
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_kv_block_table(const ps_kv* kv, int32_t seq, int32_t* pages, int32_t cap, int32_t* n) {
+  PS_TRY CHECK_KV(kv);
+  std::string e;
+  if (!n) return fail(PS_E_INVALID, "null n");
+  if (int rc = kv->meta.check_open(seq, e)) return fail(rc, e);
+  const auto& p = kv->meta.seq(seq).pages;
+  *n = (int32_t)p.size();
+  if (pages) std::memcpy(pages, p.data(), sizeof(int32_t) * std::min<size_t>(p.size(), cap > 0 ? cap : 0));
+  return PS_OK;
+  PS_CATCH
+}
+
+// ------------------------------------------------------------ call planning
+namespace {
+
+// Sequences of one call: `groups` is the list of (seq, n_new) in row order.
+struct CallSeqs {
+  std::vector<SeqInfo> si;
+  std::vector<int32_t> bt;  // compact block table
+  int32_t rows = 0;
+};
+
+ps_status plan_seqs(const ps_kv* kv, int n, const int32_t* seqs, const int32_t* n_tok, int32_t fixed_n,
+                    CallSeqs& cs) {
+  if (n < 0 || (n > 0 && !seqs)) return fail(PS_E_INVALID, "bad sequence list");
+  if (fixed_n < 0 && n > 0 && !n_tok) return fail(PS_E_INVALID, "null n_tok");
+  std::string e;
+  for (int i = 0; i < n; ++i) {
+    const int32_t s = seqs[i];
+    const int32_t nn = fixed_n >= 0 ? fixed_n : n_tok[i];
+    if (nn <= 0) return fail(PS_E_INVALID, "every sequence needs at least one new token");
+    if (int rc = kv->meta.check_writable(s, nn, e)) return fail(rc, e);
+    for (int j = 0; j < i; ++j)
+      if (seqs[j] == s) return fail(PS_E_INVALID, "sequence listed twice in one call");
+    const KvSeq& q = kv->meta.seq(s);
+    SeqInfo inf;
+    inf.kv_before = q.len;
+    inf.n_new = nn;
+    inf.row_start = cs.rows;
+    inf.bt_off = (int32_t)cs.bt.size();
+    const int32_t pages = (q.len + nn + PS_PAGE_TOKENS - 1) / PS_PAGE_TOKENS;
+    cs.bt.insert(cs.bt.end(), q.pages.begin(), q.pages.begin() + pages);
+    cs.si.push_back(inf);
+    cs.rows += nn;
+  }
+  return PS_OK;
+}
+
+struct DecodePlan {
+  std::vector<DecodeItem> items;
+  std::vector<int32_t> part_begin, part_count;
+  int32_t n_parts = 0;
+};
+
+int32_t choose_split_pages(const std::vector<SeqInfo>& si, size_t first, int n_kv, int phase) {
+  (void)phase;
+  long total = 0;
+  for (size_t b = first; b < si.size(); ++b) total += (si[b].kv_before + si[b].n_new + 15) / 16;
+  // about 2048 workgroups over the chip, at least 8 pages per split
+  const long target_items = std::max(1, 2048 / std::max(1, n_kv));
+  long sp = (total + target_items - 1) / target_items;
+  sp = std::max<long>(sp, 8);
+  sp = (sp + 3) / 4 * 4;
+  return (int32_t)sp;
+}
+
+DecodePlan plan_decode(const std::vector<SeqInfo>& si, size_t first, int32_t split_pages) {
+  DecodePlan p;
+  for (size_t b = first; b < si.size(); ++b) {
+    const int32_t np = (si[b].kv_before + si[b].n_new + 15) / 16;
+    const int32_t ns = (np + split_pages - 1) / split_pages;
+    p.part_begin.push_back(p.n_parts);
+    p.part_count.push_back(ns);
+    for (int32_t k = 0; k < ns; ++k) {
+      DecodeItem it;
+      it.b = (int32_t)(b - first);
+      it.page_begin = k * split_pages;
+      it.page_end = std::min(np, (k + 1) * split_pages);
+      it.part = p.n_parts + k;
+      p.items.push_back(it);
+    }
+    p.n_parts += ns;
+  }
+  // longest splits first
+  std::stable_sort(p.items.begin(), p.items.end(), [](const DecodeItem& a, const DecodeItem& c) {
+    return (a.page_end - a.page_begin) > (c.page_end - c.page_begin);
+  });
+  return p;
+}
+
+std::vector<PrefillItem> plan_prefill(const std::vector<SeqInfo>& si, size_t count) {
+  std::vector<PrefillItem> it;
+  for (size_t b = 0; b < count; ++b)
+    for (int32_t q0 = 0; q0 < si[b].n_new; q0 += 64) it.push_back(PrefillItem{(int32_t)b, q0});
+  // most keys first (causal imbalance)
+  std::stable_sort(it.begin(), it.end(), [&](const PrefillItem& a, const PrefillItem& c) {
+    return si[a.b].kv_before + a.q_begin > si[c.b].kv_before + c.q_begin;
+  });
+  return it;
+}
+
+bool use_mfma_attn(const ps_layer_cfg& c) { return c.dtype == PS_BF16 && c.head_dim == 128; }
+int group_of(const ps_layer_cfg& c) { return c.n_q_heads / c.n_kv_heads; }
+bool fa_ok(const ps_layer_cfg& c) { return use_mfma_attn(c) && group_of(c) % 4 == 0 && group_of(c) <= 64; }
+bool dec_ok(const ps_layer_cfg& c) {
+  const int g = group_of(c);
+  return use_mfma_attn(c) && (g == 1 || g == 2 || g == 4 || g == 8 || g == 16);
+}
+
+std::vector<double> inv_freq(const ps_layer_cfg& c) {
+  std::vector<double> f(c.head_dim / 2);
+  for (int j = 0; j < c.head_dim / 2; ++j) f[j] = std::pow(c.rope_theta, -2.0 * j / c.head_dim);
+  return f;
+}
+
+// Workspace carve-out for a layer call (after the metadata region).
+struct WsLayout {
+  size_t xn, qkv, qr, o, h, m, gemm, apart_o, apart_ml, total;
+};
+
+WsLayout layout(const ps_layer_cfg& c, size_t meta_bytes, int32_t rows, int32_t n_parts_max) {
+  const size_t eb = elt_bytes(c.dtype);
+  const size_t d = c.hidden, dq = (size_t)c.n_q_heads * c.head_dim, dkv = (size_t)c.n_kv_heads * c.head_dim;
+  WsLayout L;
+  size_t off = align_up(meta_bytes, 256);
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  L.xn = take(rows * d * eb);
+  L.qkv = take(rows * (dq + 2 * dkv) * eb);
+  L.qr = take(rows * dq * eb);
+  L.o = take(rows * dq * eb);
+  L.h = take(rows * d * 4);
+  L.m = take(rows * (size_t)c.ffn * eb);
+  size_t g = 0;
+  if (rows <= 64) {
+    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)(dq + 2 * dkv), (int)d));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)d, (int)dq));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, 2 * c.ffn, (int)d));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)d, c.ffn));
+  }
+  L.gemm = take(g);
+  L.apart_o = take((size_t)n_parts_max * dq * 4);
+  L.apart_ml = take((size_t)n_parts_max * c.n_q_heads * 2 * 4);
+  L.total = off;
+  return L;
+}
+
+size_t meta_bound(const ps_layer_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_pages) {
+  size_t b = 0;
+  b += align_up(sizeof(SeqInfo) * max_seqs, 256);
+  b += align_up(4ull * max_seqs * max_pages, 256);
+  b += align_up(8ull * c.head_dim / 2, 256);
+  const size_t parts = (size_t)max_seqs * ((max_pages + 7) / 8);
+  b += align_up(sizeof(DecodeItem) * parts, 256) + 2 * align_up(4ull * max_seqs, 256);
+  b += align_up(sizeof(PrefillItem) * ((size_t)max_rows / 64 + max_seqs), 256);
+  return b + 256;
+}
+
+ps_status check_ws(const void* ws, size_t have, size_t need) {
+  if (!ws) return fail(PS_E_INVALID, "null workspace");
+  if (have < need)
+    return fail(PS_E_INVALID, "workspace too small: " + std::to_string(have) + " < " + std::to_string(need));
+  return PS_OK;
+}
+
+ps_status check_layer(const ps_kv* kv, int layer) {
+  if (layer < 0 || layer >= kv->n_layers) return fail(PS_E_INVALID, "layer index out of range");
+  return PS_OK;
+}
+
+ps_status last_launch_error() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return PS_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ KV device ops
+extern "C" ps_status ps_kv_append(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                  const int32_t* n_tok, const void* k, const void* v, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  CallSeqs cs;
+  if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
+  if (cs.rows > 0 && (!k || !v)) return fail(PS_E_INVALID, "null k or v");
+  Meta mt;
+  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  if (ps_status rc = check_ws(ws, ws_bytes, mt.size())) return rc;
+  if (cs.rows == 0) return PS_OK;
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  char* w = (char*)ws;
+  launch_kv_append(kv->cfg.dtype, cs.rows, k, v, kv->layer_base(layer), (const SeqInfo*)(w + o_si),
+                   (const int32_t*)(w + o_bt), n_seqs, kv->cfg.n_kv_heads, kv->cfg.head_dim, st);
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k_out, void* v_out, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  std::string e;
+  if (int rc = kv->meta.check_open(seq, e)) return fail(rc, e);
+  const KvSeq& q = kv->meta.seq(seq);
+  if (q.len > 0 && (!k_out || !v_out)) return fail(PS_E_INVALID, "null output");
+  Meta mt;
+  const int32_t pages = (q.len + 15) / 16;
+  mt.add(q.pages.data(), pages * 4);
+  if (ps_status rc = check_ws(ws, ws_bytes, mt.size())) return rc;
+  if (q.len == 0) return PS_OK;
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  launch_kv_gather(kv->cfg.dtype, q.len, kv->layer_base(layer), (const int32_t*)ws, k_out, v_out,
+                   kv->cfg.n_kv_heads, kv->cfg.head_dim, st);
+  return last_launch_error();
+  PS_CATCH
+}
+
+// ------------------------------------------------------------------ layer
+extern "C" ps_status ps_layer_create(const ps_layer_cfg* c, ps_layer** out) {
+  PS_TRY
+  if (ps_status rc = check_cfg(c)) return rc;
+  if (!out) return fail(PS_E_INVALID, "null out");
+  ps_layer* L = new ps_layer;
+  L->cfg = *c;
+  *out = L;
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" ps_status ps_layer_destroy(ps_layer* L) {
+  PS_TRY
+  delete L;
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" size_t ps_workspace_bytes(const ps_layer_cfg* c, int32_t max_rows, int32_t max_seqs,
+                                     int32_t max_pages_per_seq) {
+  if (!c || max_rows < 0 || max_seqs < 0 || max_pages_per_seq < 0) return 0;
+  const size_t mb = meta_bound(*c, max_rows, max_seqs, max_pages_per_seq);
+  const int32_t parts = max_seqs * ((max_pages_per_seq + 7) / 8);
+  return layout(*c, mb, max_rows, parts).total;
+}
+
+namespace {
+
+// One layer over n_chunk prefill sequences (chunk_tok rows each) followed by
+// n_dec decode sequences (one row each).
+ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase, int32_t n_chunk,
+                    const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec, const int32_t* dec_seqs,
+                    const void* x_in, void* x_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!L) return fail(PS_E_INVALID, "null layer handle");
+  CHECK_KV(kv);
+  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm || !w->w_gate_up || !w->w_down)
+    return fail(PS_E_INVALID, "null weight pointer");
+  const ps_layer_cfg& c = L->cfg;
+  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0)
+    return fail(PS_E_INVALID, "layer and KV pool configurations differ");
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  if (phase < PS_PHASE_PREFILL || phase > PS_PHASE_ANSWER) return fail(PS_E_INVALID, "bad phase");
+
+  CallSeqs cs;
+  if (ps_status rc = plan_seqs(kv, n_chunk, chunk_seqs, chunk_tok, -1, cs)) return rc;
+  const int32_t chunk_rows = cs.rows;
+  if (ps_status rc = plan_seqs(kv, n_dec, dec_seqs, nullptr, 1, cs)) return rc;
+  for (int i = 0; i < n_dec; ++i)
+    for (int j = 0; j < n_chunk; ++j)
+      if (dec_seqs[i] == chunk_seqs[j]) return fail(PS_E_INVALID, "sequence both chunked and decoding");
+  const int32_t rows = cs.rows;
+  if (rows == 0) return PS_OK;
+  if (!x_in || !x_out) return fail(PS_E_INVALID, "null activation pointer");
+
+  const int d = c.hidden, dq = c.n_q_heads * c.head_dim, dkv = c.n_kv_heads * c.head_dim;
+  const int dt = c.dtype, G = group_of(c);
+  // every GEMM of the call must be supported before anything is enqueued
+  if (gemm_check(dt, 0, rows, dq + 2 * dkv, d) || gemm_check(dt, 1, rows, d, dq) ||
+      gemm_check(dt, 2, rows, 2 * c.ffn, d) || gemm_check(dt, 1, rows, d, c.ffn))
+    return fail(PS_E_UNSUPPORTED, "GEMM shape not supported by this build");
+
+  Meta mt;
+  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  const std::vector<double> fr = inv_freq(c);
+  const size_t o_fr = mt.add(fr.data(), fr.size() * 8);
+  const bool fa = fa_ok(c) && n_chunk > 0;
+  const bool dec_mfma = dec_ok(c) && n_dec > 0;
+  std::vector<PrefillItem> pitems;
+  size_t o_pi = 0;
+  if (fa) {
+    pitems = plan_prefill(cs.si, n_chunk);
+    o_pi = mt.add(pitems.data(), pitems.size() * sizeof(PrefillItem));
+  }
+  DecodePlan dp;
+  size_t o_di = 0, o_pb = 0, o_pc = 0;
+  if (dec_mfma) {
+    dp = plan_decode(cs.si, n_chunk, choose_split_pages(cs.si, n_chunk, c.n_kv_heads, phase));
+    o_di = mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
+    o_pb = mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
+    o_pc = mt.add(dp.part_count.data(), dp.part_count.size() * 4);
+  }
+  const WsLayout wl = layout(c, mt.size(), rows, dp.n_parts);
+  if (ps_status rc = check_ws(ws, ws_bytes, wl.total)) return rc;
+
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+
+  char* W = (char*)ws;
+  const SeqInfo* si = (const SeqInfo*)(W + o_si);
+  const int32_t* bt = (const int32_t*)(W + o_bt);
+  void* xn = W + wl.xn;
+  void* qkv = W + wl.qkv;
+  void* qr = W + wl.qr;
+  void* o = W + wl.o;
+  void* h = W + wl.h;
+  void* m = W + wl.m;
+  void* gws = W + wl.gemm;
+  const size_t gws_bytes = wl.apart_o - wl.gemm;
+  void* pool = kv->layer_base(layer);
+  const size_t eb = elt_bytes(dt);
+  const float scale = 1.0f / std::sqrt((float)c.head_dim);
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  int bad = 0;
+
+  bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st);
+  bad |= launch_gemm(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes, st);
+  bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + o_fr), (int)cs.si.size(),
+                             c.n_q_heads, c.n_kv_heads, c.head_dim, st);
+  // attention: prefill rows on the flash kernel, decode rows on the split-K
+  // kernel, anything else (fp32, other head sizes) on the vector kernel
+  if (n_chunk > 0) {
+    if (fa)
+      bad |= launch_fa_prefill(G, (int)pitems.size(), c.n_kv_heads, qr, pool, si, bt,
+                               (const PrefillItem*)(W + o_pi), o, scale_log2, st);
+    else
+      bad |= launch_attn_generic(dt, 0, chunk_rows, (int)cs.si.size(), c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
+                                 pool, si, bt, o, scale, st);
+  }
+  if (n_dec > 0) {
+    if (dec_mfma) {
+      const char* qd = (const char*)qr + (size_t)chunk_rows * dq * eb;
+      char* od = (char*)o + (size_t)chunk_rows * dq * eb;
+      bad |= launch_decode_attn(G, (int)dp.items.size(), c.n_kv_heads, n_dec, qd, pool, si + n_chunk, bt,
+                                (const DecodeItem*)(W + o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
+                                (const int32_t*)(W + o_pb), (const int32_t*)(W + o_pc), od, scale_log2, st);
+    } else {
+      bad |= launch_attn_generic(dt, chunk_rows, n_dec, (int)cs.si.size(), c.n_q_heads, c.n_kv_heads, c.head_dim,
+                                 qr, pool, si, bt, o, scale, st);
+    }
+  }
+  bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
+  bad |= launch_rmsnorm(PS_F32, dt, dt, rows, d, h, w->ffn_norm, c.rms_eps, xn, st);
+  bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes, st);
+  bad |= launch_gemm(dt, PS_F32, dt, PS_EPI_RESIDUAL, rows, d, c.ffn, m, w->w_down, h, x_out, gws, gws_bytes, st);
+  if (bad) return fail(PS_E_UNSUPPORTED, "a kernel rejected its configuration");
+  return last_launch_error();
+}
+
+}  // namespace
+
+extern "C" ps_status ps_prefill(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_seqs,
+                                const int32_t* seqs, const int32_t* n_tok, const void* x_in, void* x_out, void* ws,
+                                size_t ws_bytes, void* stream) {
+  PS_TRY
+  return run_layer(L, w, kv, layer, PS_PHASE_PREFILL, n_seqs, seqs, n_tok, 0, nullptr, x_in, x_out, ws, ws_bytes,
+                   stream);
+  PS_CATCH
+}
+
+extern "C" ps_status ps_decode_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase,
+                                    int32_t n_seqs, const int32_t* seqs, const void* x_in, void* x_out, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  PS_TRY
+  return run_layer(L, w, kv, layer, phase, 0, nullptr, nullptr, n_seqs, seqs, x_in, x_out, ws, ws_bytes, stream);
+  PS_CATCH
+}
+
+extern "C" ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_chunk,
+                                   const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec,
+                                   const int32_t* dec_seqs, const void* x_in, void* x_out, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  PS_TRY
+  return run_layer(L, w, kv, layer, PS_PHASE_THINK, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, x_in, x_out,
+                   ws, ws_bytes, stream);
+  PS_CATCH
+}
+
+// ------------------------------------------------------------------ ops
+extern "C" ps_status ps_op_rmsnorm(int32_t x_dt, int32_t g_dt, int32_t y_dt, int32_t rows, int32_t d,
+                                   const void* x, const void* g, float eps, void* y, void* stream) {
+  PS_TRY
+  if (rows < 0 || d <= 0) return fail(PS_E_INVALID, "bad shape");
+  if (rows > 0 && (!x || !g || !y)) return fail(PS_E_INVALID, "null pointer");
+  for (int dt : {x_dt, g_dt, y_dt})
+    if (dt != PS_F32 && dt != PS_BF16) return fail(PS_E_INVALID, "bad dtype");
+  if (launch_rmsnorm(x_dt, g_dt, y_dt, rows, d, x, g, eps, y, (hipStream_t)stream))
+    return fail(PS_E_UNSUPPORTED, "dtype combination not supported");
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" size_t ps_op_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K) {
+  if (M < 0 || N <= 0 || K <= 0) return 0;
+  return gemm_workspace_bytes(dtype, M, N, K);
+}
+
+extern "C" ps_status ps_op_gemm(int32_t dtype, int32_t r_dt, int32_t c_dt, int32_t epi, int32_t M, int32_t N,
+                                int32_t K, const void* A, const void* Wt, const void* R, void* C, void* ws,
+                                size_t ws_bytes, void* stream) {
+  PS_TRY
+  if (epi < 0 || epi > 2) return fail(PS_E_INVALID, "bad epilogue");
+  if (M > 0 && (!A || !Wt || !C || (epi == 1 && !R))) return fail(PS_E_INVALID, "null pointer");
+  if (gemm_check(dtype, epi, M, N, K)) return fail(PS_E_UNSUPPORTED, "GEMM shape not supported");
+  const size_t need = gemm_workspace_bytes(dtype, M, N, K);
+  if (need && (!ws || ws_bytes < need)) return fail(PS_E_INVALID, "workspace too small for split-K partials");
+  if (epi != 1) r_dt = 0;
+  int rc = launch_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, Wt, R, C, ws, ws_bytes, (hipStream_t)stream);
+  if (rc) return fail(PS_E_UNSUPPORTED, "dtype/epilogue combination not supported");
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_rope_kvwrite(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                        const int32_t* n_tok, const void* qkv, void* q_out, void* ws,
+                                        size_t ws_bytes, void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  CallSeqs cs;
+  if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
+  if (cs.rows > 0 && (!qkv || !q_out)) return fail(PS_E_INVALID, "null pointer");
+  Meta mt;
+  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  const std::vector<double> fr = inv_freq(kv->cfg);
+  const size_t o_fr = mt.add(fr.data(), fr.size() * 8);
+  if (ps_status rc = check_ws(ws, ws_bytes, mt.size())) return rc;
+  if (cs.rows == 0) return PS_OK;
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  char* W = (char*)ws;
+  const ps_layer_cfg& c = kv->cfg;
+  launch_rope_kvwrite(c.dtype, cs.rows, qkv, q_out, kv->layer_base(layer), (const SeqInfo*)(W + o_si),
+                      (const int32_t*)(W + o_bt), (const double*)(W + o_fr), n_seqs, c.n_q_heads, c.n_kv_heads,
+                      c.head_dim, st);
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                     const int32_t* n_tok, const void* q, void* o, void* ws, size_t ws_bytes,
+                                     void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  CallSeqs cs;
+  if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
+  if (cs.rows > 0 && (!q || !o)) return fail(PS_E_INVALID, "null pointer");
+  const ps_layer_cfg& c = kv->cfg;
+  Meta mt;
+  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  const bool fa = fa_ok(c);
+  std::vector<PrefillItem> pitems;
+  size_t o_pi = 0;
+  if (fa) {
+    pitems = plan_prefill(cs.si, cs.si.size());
+    o_pi = mt.add(pitems.data(), pitems.size() * sizeof(PrefillItem));
+  }
+  if (ps_status rc = check_ws(ws, ws_bytes, mt.size())) return rc;
+  if (cs.rows == 0) return PS_OK;
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  char* W = (char*)ws;
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  int bad;
+  if (fa)
+    bad = launch_fa_prefill(group_of(c), (int)pitems.size(), c.n_kv_heads, q, kv->layer_base(layer),
+                            (const SeqInfo*)(W + o_si), (const int32_t*)(W + o_bt), (const PrefillItem*)(W + o_pi), o,
+                            scale_log2, st);
+  else
+    bad = launch_attn_generic(c.dtype, 0, cs.rows, n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, q,
+                              kv->layer_base(layer), (const SeqInfo*)(W + o_si), (const int32_t*)(W + o_bt), o,
+                              1.0f / std::sqrt((float)c.head_dim), st);
+  if (bad) return fail(PS_E_UNSUPPORTED, "attention configuration not supported");
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                            const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
+                                            void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  const ps_layer_cfg& c = kv->cfg;
+  if (!dec_ok(c)) return fail(PS_E_UNSUPPORTED, "split-K decode attention needs bf16, head_dim 128, G <= 16");
+  if (split_pages < 0) return fail(PS_E_INVALID, "negative split_pages");
+  CallSeqs cs;
+  if (ps_status rc = plan_seqs(kv, n_seqs, seqs, nullptr, 1, cs)) return rc;
+  if (n_seqs > 0 && (!q || !o)) return fail(PS_E_INVALID, "null pointer");
+  Meta mt;
+  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  const int32_t sp = split_pages > 0 ? split_pages : choose_split_pages(cs.si, 0, c.n_kv_heads, PS_PHASE_ANSWER);
+  DecodePlan dp = plan_decode(cs.si, 0, sp);
+  const size_t o_di = mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
+  const size_t o_pb = mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
+  const size_t o_pc = mt.add(dp.part_count.data(), dp.part_count.size() * 4);
+  const size_t dq = (size_t)c.n_q_heads * c.head_dim;
+  const size_t off_po = mt.size();
+  const size_t off_pml = align_up(off_po + (size_t)dp.n_parts * dq * 4, 256);
+  const size_t need = align_up(off_pml + (size_t)dp.n_parts * c.n_q_heads * 2 * 4, 256);
+  if (ps_status rc = check_ws(ws, ws_bytes, need)) return rc;
+  if (n_seqs == 0) return PS_OK;
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  char* W = (char*)ws;
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  int bad = launch_decode_attn(group_of(c), (int)dp.items.size(), c.n_kv_heads, n_seqs, q, kv->layer_base(layer),
+                               (const SeqInfo*)(W + o_si), (const int32_t*)(W + o_bt),
+                               (const DecodeItem*)(W + o_di), (float*)(W + off_po), (float*)(W + off_pml),
+                               (const int32_t*)(W + o_pb), (const int32_t*)(W + o_pc), o, scale_log2, st);
+  if (bad) return fail(PS_E_UNSUPPORTED, "decode attention configuration not supported");
+  return last_launch_error();
+  PS_CATCH
+}

@@ -1,0 +1,67 @@
+// Shared device/host definitions for the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ps {
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kPageTokens = 16;
+constexpr int kGateUpBlock = 32;
+
+__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// float -> bf16 bits, round to nearest even (finite inputs; NaN kept quiet).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+template <typename T> struct Elt;
+template <> struct Elt<float> {
+  __device__ static float load(const float* p, long i) { return p[i]; }
+  __device__ static void store(float* p, long i, float v) { p[i] = v; }
+};
+template <> struct Elt<bf16_t> {
+  __device__ static float load(const bf16_t* p, long i) { return bf2f(p[i]); }
+  __device__ static void store(bf16_t* p, long i, float v) { p[i] = f2bf(v); }
+};
+
+// Per-call sequence record uploaded with the call's metadata.
+struct SeqInfo {
+  int32_t kv_before;  // committed length before this call (first new position)
+  int32_t n_new;      // rows this call adds for the sequence
+  int32_t row_start;  // first row of the sequence in the call's activations
+  int32_t bt_off;     // offset of its block-table row in the compact table
+};
+
+// One split of decode attention: logical pages [page_begin, page_end) of
+// batch entry b; part is the index of its partial result.
+struct DecodeItem {
+  int32_t b;
+  int32_t page_begin;
+  int32_t page_end;
+  int32_t part;
+};
+
+// One query tile of prefill attention.
+struct PrefillItem {
+  int32_t b;
+  int32_t q_begin;  // first new row of the tile, relative to the sequence's new rows
+};
+
+}  // namespace ps

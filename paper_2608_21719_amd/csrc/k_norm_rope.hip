@@ -1,0 +1,262 @@
+// RMSNorm, RoPE + paged KV write, KV append and KV gather (gfx950).
+//
+// All four are HBM-bound streaming kernels: one row (token) per workgroup,
+// fp32 arithmetic, coalesced row reads.
+#include "common.h"
+#include "launch.h"
+
+namespace ps {
+
+// ---------------------------------------------------------------- RMSNorm
+// y = x / sqrt(mean(x^2) + eps) * g, one row per 256-thread workgroup.
+template <typename TX, typename TG, typename TY>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const TX* __restrict__ x, const TG* __restrict__ g,
+                                                      TY* __restrict__ y, int d, float eps) {
+  const long row = blockIdx.x;
+  const TX* xr = x + row * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = Elt<TX>::load(xr, i);
+    ss += v * v;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = red[0] + red[1] + red[2] + red[3];
+  float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  TY* yr = y + row * d;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    Elt<TY>::store(yr, i, Elt<TX>::load(xr, i) * inv * Elt<TG>::load(g, i));
+  }
+}
+
+// Vectorised bf16 -> bf16 variant: 8 elements per 16-byte access, the row
+// kept in registers between the two passes (d <= 256 * 8 * VPT).
+template <typename TX, int VPT>
+__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const TX* __restrict__ x, const bf16_t* __restrict__ g,
+                                                          bf16_t* __restrict__ y, int d, float eps) {
+  const long row = blockIdx.x;
+  float v[VPT][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < VPT; ++c) {
+    int i = (c * 256 + threadIdx.x) * 8;
+    if (i < d) {
+      if constexpr (sizeof(TX) == 2) {
+        uint4 w = *(const uint4*)(x + row * d + i);
+        uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[c][2 * e] = bf_lo(ws[e]);
+          v[c][2 * e + 1] = bf_hi(ws[e]);
+        }
+      } else {
+        float4 a = *(const float4*)(x + row * d + i);
+        float4 b = *(const float4*)(x + row * d + i + 4);
+        v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
+        v[c][4] = b.x; v[c][5] = b.y; v[c][6] = b.z; v[c][7] = b.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[c][e] * v[c][e];
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = red[0] + red[1] + red[2] + red[3];
+  float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int c = 0; c < VPT; ++c) {
+    int i = (c * 256 + threadIdx.x) * 8;
+    if (i < d) {
+      uint4 gw = *(const uint4*)(g + i);
+      uint32_t gs[4] = {gw.x, gw.y, gw.z, gw.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = pack_bf2(v[c][2 * e] * inv * bf_lo(gs[e]), v[c][2 * e + 1] * inv * bf_hi(gs[e]));
+      *(uint4*)(y + row * d + i) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
+                   void* y, hipStream_t st) {
+  if (rows == 0) return 0;
+  dim3 grid(rows), block(256);
+  if (g_dt == 1 && y_dt == 1 && d % 8 == 0 && d <= 256 * 8 * 4) {
+    if (x_dt == 1) {
+      hipLaunchKernelGGL((rmsnorm_vec_kernel<bf16_t, 4>), grid, block, 0, st, (const bf16_t*)x,
+                         (const bf16_t*)g, (bf16_t*)y, d, eps);
+    } else {
+      hipLaunchKernelGGL((rmsnorm_vec_kernel<float, 4>), grid, block, 0, st, (const float*)x,
+                         (const bf16_t*)g, (bf16_t*)y, d, eps);
+    }
+    return 0;
+  }
+#define RMS_CASE(TX_, TG_, TY_, a, b, c)                                                           \
+  if (x_dt == a && g_dt == b && y_dt == c) {                                                       \
+    hipLaunchKernelGGL((rmsnorm_kernel<TX_, TG_, TY_>), grid, block, 0, st, (const TX_*)x,        \
+                       (const TG_*)g, (TY_*)y, d, eps);                                           \
+    return 0;                                                                                      \
+  }
+  RMS_CASE(float, float, float, 0, 0, 0)
+  RMS_CASE(float, float, bf16_t, 0, 0, 1)
+  RMS_CASE(bf16_t, bf16_t, bf16_t, 1, 1, 1)
+  RMS_CASE(bf16_t, bf16_t, float, 1, 1, 0)
+  RMS_CASE(float, bf16_t, bf16_t, 0, 1, 1)
+  RMS_CASE(float, bf16_t, float, 0, 1, 0)
+  RMS_CASE(bf16_t, float, float, 1, 0, 0)
+  RMS_CASE(bf16_t, float, bf16_t, 1, 0, 1)
+#undef RMS_CASE
+  return -1;
+}
+
+// ---------------------------------------------------------------- paging
+// Element offset of the K row of (page, kv head, slot) within a layer, and
+// of the V^T column. Page block per (page, kv head): K [16][hd] then
+// V^T [hd][16].
+__device__ __forceinline__ long kv_block(int page, int kvh, int n_kv, int hd) {
+  return ((long)page * n_kv + kvh) * (2L * kPageTokens * hd);
+}
+
+__device__ __forceinline__ int find_seq(const SeqInfo* __restrict__ si, int n_seqs, int row) {
+  int lo = 0, hi = n_seqs - 1;
+  while (lo < hi) {  // last b with row_start <= row
+    int mid = (lo + hi + 1) >> 1;
+    if (si[mid].row_start <= row) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ---------------------------------------------------------------- RoPE + KV
+// One row per workgroup: rotate the row's q and k heads (rotate-half, angle
+// pos * inv_freq[j] evaluated in fp64), write q to q_out and k, v into the
+// row's page slot.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__ qkv, T* __restrict__ q_out,
+                                                           T* __restrict__ pool, const SeqInfo* __restrict__ si,
+                                                           const int32_t* __restrict__ bt,
+                                                           const double* __restrict__ inv_freq, int n_seqs,
+                                                           int n_q, int n_kv, int hd) {
+  const int row = blockIdx.x;
+  const int half = hd >> 1;
+  __shared__ float cs[64], sn[64];
+  const int b = find_seq(si, n_seqs, row);
+  const SeqInfo s = si[b];
+  const int pos = s.kv_before + (row - s.row_start);
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    double a = (double)pos * inv_freq[j];
+    double sv, cv;
+    sincos(a, &sv, &cv);
+    cs[j] = (float)cv;
+    sn[j] = (float)sv;
+  }
+  __syncthreads();
+  const int dqkv = (n_q + 2 * n_kv) * hd;
+  const T* xr = qkv + (long)row * dqkv;
+  const int page = bt[s.bt_off + pos / kPageTokens];
+  const int slot = pos % kPageTokens;
+  // q and k: rotate pairs (j, j + half)
+  for (int idx = threadIdx.x; idx < (n_q + n_kv) * half; idx += blockDim.x) {
+    int head = idx / half, j = idx - head * half;
+    float x1 = Elt<T>::load(xr, head * hd + j);
+    float x2 = Elt<T>::load(xr, head * hd + j + half);
+    float y1 = x1 * cs[j] - x2 * sn[j];
+    float y2 = x2 * cs[j] + x1 * sn[j];
+    if (head < n_q) {
+      Elt<T>::store(q_out, (long)row * n_q * hd + head * hd + j, y1);
+      Elt<T>::store(q_out, (long)row * n_q * hd + head * hd + j + half, y2);
+    } else {
+      long base = kv_block(page, head - n_q, n_kv, hd) + (long)slot * hd;
+      Elt<T>::store(pool, base + j, y1);
+      Elt<T>::store(pool, base + j + half, y2);
+    }
+  }
+  // v: stored dimension-major within the page
+  for (int idx = threadIdx.x; idx < n_kv * hd; idx += blockDim.x) {
+    int kvh = idx / hd, dim = idx - kvh * hd;
+    T v = xr[(n_q + n_kv) * hd + idx];
+    pool[kv_block(page, kvh, n_kv, hd) + (long)kPageTokens * hd + (long)dim * kPageTokens + slot] = v;
+  }
+}
+
+int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* pool_layer, const SeqInfo* si,
+                        const int32_t* bt, const double* inv_freq, int n_seqs, int n_q, int n_kv, int hd,
+                        hipStream_t st) {
+  if (rows == 0) return 0;
+  if (hd > 128) return -1;
+  if (dt == 1)
+    hipLaunchKernelGGL(rope_kvwrite_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, (const bf16_t*)qkv,
+                       (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd);
+  else
+    hipLaunchKernelGGL(rope_kvwrite_kernel<float>, dim3(rows), dim3(256), 0, st, (const float*)qkv,
+                       (float*)q_out, (float*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd);
+  return 0;
+}
+
+// ---------------------------------------------------------------- append
+// Caller K/V rows [rows, n_kv, hd] into their page slots (no rotation).
+template <typename T>
+__global__ __launch_bounds__(256) void kv_append_kernel(const T* __restrict__ k, const T* __restrict__ v,
+                                                        T* __restrict__ pool, const SeqInfo* __restrict__ si,
+                                                        const int32_t* __restrict__ bt, int n_seqs, int n_kv,
+                                                        int hd) {
+  const int row = blockIdx.x;
+  const int b = find_seq(si, n_seqs, row);
+  const SeqInfo s = si[b];
+  const int pos = s.kv_before + (row - s.row_start);
+  const int page = bt[s.bt_off + pos / kPageTokens];
+  const int slot = pos % kPageTokens;
+  for (int idx = threadIdx.x; idx < n_kv * hd; idx += blockDim.x) {
+    int kvh = idx / hd, dim = idx - kvh * hd;
+    long base = kv_block(page, kvh, n_kv, hd);
+    pool[base + (long)slot * hd + dim] = k[(long)row * n_kv * hd + idx];
+    pool[base + (long)kPageTokens * hd + (long)dim * kPageTokens + slot] = v[(long)row * n_kv * hd + idx];
+  }
+}
+
+int launch_kv_append(int dt, int rows, const void* k, const void* v, void* pool_layer, const SeqInfo* si,
+                     const int32_t* bt, int n_seqs, int n_kv, int hd, hipStream_t st) {
+  if (rows == 0) return 0;
+  if (dt == 1)
+    hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, (const bf16_t*)k,
+                       (const bf16_t*)v, (bf16_t*)pool_layer, si, bt, n_seqs, n_kv, hd);
+  else
+    hipLaunchKernelGGL(kv_append_kernel<float>, dim3(rows), dim3(256), 0, st, (const float*)k,
+                       (const float*)v, (float*)pool_layer, si, bt, n_seqs, n_kv, hd);
+  return 0;
+}
+
+// ---------------------------------------------------------------- gather
+// Positions [0, len) of one sequence into contiguous [len, n_kv, hd].
+template <typename T>
+__global__ __launch_bounds__(256) void kv_gather_kernel(const T* __restrict__ pool, const int32_t* __restrict__ bt,
+                                                        T* __restrict__ k_out, T* __restrict__ v_out, int n_kv,
+                                                        int hd) {
+  const int pos = blockIdx.x;
+  const int page = bt[pos / kPageTokens];
+  const int slot = pos % kPageTokens;
+  for (int idx = threadIdx.x; idx < n_kv * hd; idx += blockDim.x) {
+    int kvh = idx / hd, dim = idx - kvh * hd;
+    long base = kv_block(page, kvh, n_kv, hd);
+    k_out[(long)pos * n_kv * hd + idx] = pool[base + (long)slot * hd + dim];
+    v_out[(long)pos * n_kv * hd + idx] = pool[base + (long)kPageTokens * hd + (long)dim * kPageTokens + slot];
+  }
+}
+
+int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt, void* k_out, void* v_out,
+                     int n_kv, int hd, hipStream_t st) {
+  if (len == 0) return 0;
+  if (dt == 1)
+    hipLaunchKernelGGL(kv_gather_kernel<bf16_t>, dim3(len), dim3(256), 0, st, (const bf16_t*)pool_layer, bt,
+                       (bf16_t*)k_out, (bf16_t*)v_out, n_kv, hd);
+  else
+    hipLaunchKernelGGL(kv_gather_kernel<float>, dim3(len), dim3(256), 0, st, (const float*)pool_layer, bt,
+                       (float*)k_out, (float*)v_out, n_kv, hd);
+  return 0;
+}
+
+}  // namespace ps

@@ -1,0 +1,41 @@
+// Host-side launchers of the gfx950 kernels. Each returns 0 when the launch
+// was enqueued, a negative value for a configuration it does not support.
+// Shapes are validated by the caller (the C ABI layer) before any launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "common.h"
+
+namespace ps {
+
+// dtype codes: 0 = fp32, 1 = bf16
+int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
+                   void* y, hipStream_t st);
+
+int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* pool_layer, const SeqInfo* si,
+                        const int32_t* bt, const double* inv_freq, int n_seqs, int n_q, int n_kv, int hd,
+                        hipStream_t st);
+int launch_kv_append(int dt, int rows, const void* k, const void* v, void* pool_layer, const SeqInfo* si,
+                     const int32_t* bt, int n_seqs, int n_kv, int hd, hipStream_t st);
+int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt, void* k_out, void* v_out,
+                     int n_kv, int hd, hipStream_t st);
+
+int launch_decode_attn(int G, int n_items, int n_kv, int n_seqs, const void* q, const void* pool_layer,
+                       const SeqInfo* si, const int32_t* bt, const DecodeItem* items, float* part_o,
+                       float* part_ml, const int32_t* part_begin, const int32_t* part_count, void* o,
+                       float scale_log2, hipStream_t st);
+int launch_attn_generic(int dt, int row0, int rows, int n_seqs, int n_q, int n_kv, int hd, const void* q,
+                        const void* pool_layer, const SeqInfo* si, const int32_t* bt, void* o, float scale,
+                        hipStream_t st);
+int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
+                      const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st);
+
+// GEMM C = epi(A W^T); ws holds split-K partials for decode-sized M.
+int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
+                const void* R, void* C, void* ws, size_t ws_bytes, hipStream_t st);
+size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
+int gemm_skinny_splits(int M, int N, int K);
+int gemm_check(int dtype, int epi, int M, int N, int K);
+
+}  // namespace ps

@@ -1,0 +1,170 @@
+"""The C ABI without a GPU: exported symbols and the host-side KV pool logic."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_21719_amd import binding as B
+from synth.configs import CONFIGS
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "ps.h")
+FAKE_POOL = 0x10000  # never dereferenced by host-only calls
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ps_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported():
+    names = declared_functions()
+    assert len(names) >= 25
+    missing = [n for n in names if not hasattr(B.lib, n)]
+    assert not missing, missing
+
+
+def test_binding_covers_every_declared_function():
+    assert set(declared_functions()) == set(B._SIGS)
+
+
+def _kv(n_pages=64, max_seqs=4, max_pages=16, seed=0):
+    cfg = B.make_cfg(CONFIGS["tiny_f32"].shape)
+    return B.KV(cfg, 1, n_pages, max_seqs, max_pages, FAKE_POOL, seed)
+
+
+def test_reserve_commit_truncate_free_cycle():
+    kv = _kv()
+    s = kv.open()
+    assert kv.seq_len(s) == 0 and kv.capacity(s) == 0
+    kv.alloc(s, 17)
+    assert kv.capacity(s) == 32 and kv.free_pages() == 62
+    kv.commit([s], [17])
+    assert kv.seq_len(s) == 17
+    kv.alloc(s, 15)          # 17 + 15 = 32 fits the 2 pages already held
+    assert kv.free_pages() == 62
+    kv.alloc(s, 16)
+    assert kv.capacity(s) == 48
+    kv.truncate(s, 5)
+    assert kv.seq_len(s) == 5 and kv.capacity(s) == 48
+    kv.free(s)
+    assert kv.free_pages() == 64
+    with pytest.raises(B.PsError) as e:
+        kv.seq_len(s)
+    assert e.value.code == B.PS_E_INVALID
+
+
+def test_identity_and_shuffled_page_order():
+    kv = _kv(seed=0)
+    s = kv.open()
+    kv.alloc(s, 16 * 5)
+    assert kv.block_table(s) == [0, 1, 2, 3, 4]
+    kv2 = _kv(seed=12345)
+    s2 = kv2.open()
+    kv2.alloc(s2, 16 * 16)
+    bt = kv2.block_table(s2)
+    assert sorted(bt) == sorted(set(bt)) and len(bt) == 16 and bt != list(range(16))
+    # deterministic for a given seed
+    kv3 = _kv(seed=12345)
+    s3 = kv3.open()
+    kv3.alloc(s3, 16 * 16)
+    assert kv3.block_table(s3) == bt
+
+
+def test_pages_are_recycled_and_never_shared():
+    kv = _kv(n_pages=8, max_seqs=4, max_pages=8, seed=7)
+    a, b = kv.open(), kv.open()
+    kv.alloc(a, 48)
+    kv.alloc(b, 64)
+    assert not set(kv.block_table(a)) & set(kv.block_table(b))
+    assert kv.free_pages() == 1
+    kv.free(a)
+    c = kv.open()
+    kv.alloc(c, 64)
+    assert not set(kv.block_table(c)) & set(kv.block_table(b))
+
+
+def test_exhaustion_fails_without_side_effects():
+    kv = _kv(n_pages=4, max_seqs=2, max_pages=16)
+    s = kv.open()
+    kv.alloc(s, 40)
+    before = (kv.block_table(s), kv.free_pages(), kv.capacity(s))
+    with pytest.raises(B.PsError) as e:
+        kv.alloc(s, 100)
+    assert e.value.code == B.PS_E_NO_PAGES
+    assert (kv.block_table(s), kv.free_pages(), kv.capacity(s)) == before
+
+
+def test_per_sequence_page_limit():
+    kv = _kv(n_pages=64, max_pages=3)
+    s = kv.open()
+    with pytest.raises(B.PsError) as e:
+        kv.alloc(s, 49)
+    assert e.value.code == B.PS_E_CAPACITY
+    assert kv.free_pages() == 64
+
+
+def test_commit_is_all_or_nothing():
+    kv = _kv()
+    a, b = kv.open(), kv.open()
+    kv.alloc(a, 16)
+    kv.alloc(b, 16)
+    with pytest.raises(B.PsError) as e:
+        kv.commit([a, b], [10, 17])
+    assert e.value.code == B.PS_E_CAPACITY
+    assert kv.seq_len(a) == 0 and kv.seq_len(b) == 0
+    with pytest.raises(B.PsError):
+        kv.commit([a, a], [1, 1])
+    assert kv.seq_len(a) == 0
+
+
+def test_bad_arguments_are_rejected():
+    kv = _kv(max_seqs=1)
+    s = kv.open()
+    with pytest.raises(B.PsError) as e:
+        kv.open()
+    assert e.value.code == B.PS_E_CAPACITY
+    with pytest.raises(B.PsError):
+        kv.truncate(s, 1)
+    with pytest.raises(B.PsError):
+        kv.alloc(s, -1)
+    cfg = B.make_cfg(CONFIGS["tiny_f32"].shape)
+    cfg.n_kv_heads = 3
+    with pytest.raises(B.PsError):
+        B.KV(cfg, 1, 8, 1, 1, FAKE_POOL)
+
+
+def test_device_calls_validate_before_touching_the_device():
+    """Capacity errors surface on the host, before any launch (no GPU here)."""
+    kv = _kv()
+    s = kv.open()
+    kv.alloc(s, 16)
+    import ctypes
+    ws = np.zeros(1 << 16, np.uint8)
+    rc = B.lib.ps_kv_append(kv.h, 0, 1, B.ints([s]), B.ints([17]), ws.ctypes.data, ws.ctypes.data,
+                            ws.ctypes.data, ws.nbytes, None)
+    assert rc == B.PS_E_CAPACITY
+    rc = B.lib.ps_kv_append(kv.h, 3, 1, B.ints([s]), B.ints([1]), ws.ctypes.data, ws.ctypes.data,
+                            ws.ctypes.data, ws.nbytes, None)
+    assert rc == B.PS_E_INVALID
+    assert kv.seq_len(s) == 0
+    del ctypes
+
+
+def test_pack_gate_up_layout():
+    F, d = 64, 3
+    wg = np.arange(F * d, dtype=np.float32).reshape(F, d)
+    wu = -wg
+    out = B.pack_gate_up(wg, wu)
+    np.testing.assert_array_equal(out[0:32], wg[0:32])
+    np.testing.assert_array_equal(out[32:64], wu[0:32])
+    np.testing.assert_array_equal(out[64:96], wg[32:64])
+    np.testing.assert_array_equal(out[96:128], wu[32:64])
+
+
+def test_workspace_and_pool_sizes():
+    sh = CONFIGS["llama8b_decode"].shape
+    cfg = B.make_cfg(sh)
+    assert B.KV.pool_bytes(cfg, 1, 10) == 10 * 8 * 2 * 16 * 128 * 2
+    assert B.Layer.workspace_bytes(cfg, 64, 64, 300) > 64 * (4096 + 14336) * 2

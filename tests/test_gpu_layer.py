@@ -1,0 +1,174 @@
+"""End-to-end layer parity against the fp64 oracle (GPU).
+
+fp32 layer: elementwise |g - r| <= 1e-4 + 1e-4 |r|. bf16 layers: normwise
+max|g - r| / max|r| <= 1e-2 and rms(g - r) / rms(r) <= 1e-2 (the oracle
+rounds nowhere; bf16 rounding of GEMM inputs alone gives ~5e-3).
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as O
+from synth import gen
+from synth.configs import CONFIGS
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_21719_amd import binding as B  # noqa: E402
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+class Harness:
+    def __init__(self, wl, n_pages, max_seqs, max_pages, seed=None, max_rows=1024):
+        self.wl = wl
+        self.shape = wl.shape
+        self.dt = wl.shape.dtype
+        self.w = gen.layer_weights(wl, 0)
+        self.wf = H.weights_f64(self.w, self.dt)
+        self.dev = H.DeviceLayer(self.w, self.dt)
+        self.pool = H.Pool(self.shape, n_pages, max_seqs, max_pages,
+                           seed=gen.page_order_seed(wl) if seed is None else seed)
+        self.kv = self.pool.kv
+        self.layer = B.Layer(self.pool.cfg)
+        self.ws = H.workspace(B.Layer.workspace_bytes(self.pool.cfg, max_rows, max_seqs, max_pages))
+        self.hist = {}  # oracle-side K, V per sequence
+
+    def open(self, reserve):
+        s = self.kv.open()
+        self.kv.alloc(s, reserve)
+        sh = self.shape
+        self.hist[s] = (np.zeros((0, sh.n_kv, sh.head_dim)), np.zeros((0, sh.n_kv, sh.head_dim)))
+        return s
+
+    def oracle(self, s, x_rows):
+        kh, vh = self.hist[s]
+        r = O.layer_sequence(self.wf, self.shape, x_rows, kh, vh)
+        self.hist[s] = (np.concatenate([kh, r["k"]]), np.concatenate([vh, r["v"]]))
+        return r["out"]
+
+    def prefill(self, seqs, n_tok, x):
+        out = H.empty((x.shape[0], self.shape.hidden), self.dt)
+        self.layer.prefill(self.dev.w, self.kv, 0, seqs, n_tok, H.to_dev(x, self.dt), out, self.ws)
+        self.kv.commit(seqs, n_tok)
+        sync()
+        return H.to_f64(out)
+
+    def decode(self, seqs, x, phase=B.PS_PHASE_ANSWER):
+        out = H.empty((x.shape[0], self.shape.hidden), self.dt)
+        self.layer.decode_step(self.dev.w, self.kv, 0, phase, seqs, H.to_dev(x, self.dt), out, self.ws)
+        self.kv.commit(seqs, [1] * len(seqs))
+        sync()
+        return H.to_f64(out)
+
+
+def check(got, ref, dt, what):
+    if dt == "f32":
+        H.assert_close_elementwise(got, ref, H.F32_TOL_ABS, H.F32_TOL_REL, what)
+    else:
+        mx, rms = H.normwise(got, ref)
+        assert mx <= H.NORMWISE_TOL and rms <= H.NORMWISE_TOL, f"{what}: normwise max {mx:.2e} rms {rms:.2e}"
+
+
+def test_tiny_fp32_prefill_then_16_decode_steps():
+    """The tiny fp32 workload in full: 4 x 128 prefill, 16 decode steps, shuffled pages."""
+    wl = CONFIGS["tiny_f32"]
+    h = Harness(wl, n_pages=64, max_seqs=4, max_pages=16)
+    T, B_ = wl.prefill_tokens, wl.prefill_seqs
+    seqs = [h.open(T + wl.decode_steps) for _ in range(B_)]
+    x = gen.prefill_input(wl, T * B_)
+    got = h.prefill(seqs, [T] * B_, x)
+    xf = gen.widen(x, "f32")
+    for i, s in enumerate(seqs):
+        check(got[i * T:(i + 1) * T], h.oracle(s, xf[i * T:(i + 1) * T]), "f32", f"prefill seq {i}")
+    for step in range(wl.decode_steps):
+        xd = gen.decode_input(wl, B_, step)
+        got = h.decode(seqs, xd)
+        xdf = gen.widen(xd, "f32")
+        ref = np.concatenate([h.oracle(s, xdf[i:i + 1]) for i, s in enumerate(seqs)])
+        check(got, ref, "f32", f"decode step {step}")
+
+
+@pytest.fixture(scope="module")
+def h8():
+    return Harness(CONFIGS["llama8b_prefill"], n_pages=512, max_seqs=16, max_pages=64)
+
+
+def test_8b_layer_prefill_then_decode(h8):
+    h = h8
+    lens = [100, 37, 64]
+    seqs = [h.open(L + 3) for L in lens]
+    x = gen.prefill_input(h.wl, sum(lens), step=1)
+    got = h.prefill(seqs, lens, x)
+    xf = gen.widen(x, "bf16")
+    r0 = 0
+    for s, L in zip(seqs, lens):
+        check(got[r0:r0 + L], h.oracle(s, xf[r0:r0 + L]), "bf16", f"prefill L={L}")
+        r0 += L
+    for step in range(3):
+        xd = gen.decode_input(h.wl, len(seqs), 10 + step)
+        got = h.decode(seqs, xd, B.PS_PHASE_THINK)
+        xdf = gen.widen(xd, "bf16")
+        ref = np.concatenate([h.oracle(s, xdf[i:i + 1]) for i, s in enumerate(seqs)])
+        check(got, ref, "bf16", f"decode step {step}")
+    for s in seqs:
+        h.kv.free(s)
+
+
+def test_8b_decode_equals_last_row_of_prefill(h8):
+    """Two kernels paths, same inputs: prefill of T+1 rows vs prefill T + decode 1."""
+    h = h8
+    T = 70
+    x = gen.prefill_input(h.wl, T + 1, step=2)
+    a = h.open(T + 1)
+    b = h.open(T + 1)
+    full = h.prefill([a], [T + 1], x)
+    h.prefill([b], [T], x[:T])
+    dec = h.decode([b], x[T:T + 1])
+    H.assert_close_elementwise(dec[0], full[T], H.BF16_TOL_ABS, H.BF16_TOL_REL, "decode vs prefill row")
+    for s in (a, b):
+        h.kv.free(s)
+
+
+def test_8b_mixed_step_matches_oracle(h8):
+    """Chunked prefill (fresh and with a cached prefix) fused with decodes."""
+    h = h8
+    c_new = h.open(48)
+    c_pre = h.open(20 + 33)
+    d1 = h.open(90)
+    d2 = h.open(20)
+    xp = gen.prefill_input(h.wl, 20 + 80 + 17, step=3)
+    xpf = gen.widen(xp, "bf16")
+    h.prefill([c_pre, d1, d2], [20, 80, 17], xp)
+    for s, (r0, n) in zip([c_pre, d1, d2], [(0, 20), (20, 80), (100, 17)]):
+        h.oracle(s, xpf[r0:r0 + n])
+    xm = gen.mixed_input(h.wl, 48 + 33 + 2)
+    xmf = gen.widen(xm, "bf16")
+    out = H.empty((83, h.shape.hidden), "bf16")
+    h.layer.mixed_step(h.dev.w, h.kv, 0, [c_new, c_pre], [48, 33], [d1, d2], H.to_dev(xm, "bf16"), out, h.ws)
+    h.kv.commit([c_new, c_pre, d1, d2], [48, 33, 1, 1])
+    sync()
+    got = H.to_f64(out)
+    check(got[:48], h.oracle(c_new, xmf[:48]), "bf16", "mixed chunk fresh")
+    check(got[48:81], h.oracle(c_pre, xmf[48:81]), "bf16", "mixed chunk with prefix")
+    check(got[81:82], h.oracle(d1, xmf[81:82]), "bf16", "mixed decode 1")
+    check(got[82:83], h.oracle(d2, xmf[82:83]), "bf16", "mixed decode 2")
+    for s in (c_new, c_pre, d1, d2):
+        h.kv.free(s)
+
+
+def test_layer_rejects_capacity_overrun_without_launching(h8):
+    h = h8
+    s = h.open(16)
+    x = gen.prefill_input(h.wl, 17)
+    with pytest.raises(B.PsError) as e:
+        h.prefill([s], [17], x)
+    assert e.value.code == B.PS_E_CAPACITY
+    assert h.kv.seq_len(s) == 0
+    h.kv.free(s)
