@@ -46,6 +46,14 @@ class LayerW(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise LibraryMissing(f"{LIB_PATH} is not built; run `python -m paper_2608_21719_amd.build`")
+    # torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
+    # Load it first so that libps binds to the runtime that owns torch's
+    # device allocations and streams; a second runtime in the process would
+    # not see the device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     return ctypes.CDLL(LIB_PATH)
 
 
