@@ -1,0 +1,267 @@
+"""Benchmark of the layer hot path on one MI355X.
+
+Headline (``value``): prefill tokens/s of the 8B-shaped layer on 8 prompts x
+2048 tokens (one step = one ps_prefill over the batch: RMSNorm, QKV GEMM,
+RoPE + paged KV write, causal flash attention, O GEMM + residual, RMSNorm,
+gate_up GEMM + SwiGLU, down GEMM + residual). The ``decode`` object holds the
+8B-shaped decode phase: batch 64, contexts U{1024..4096}, one ps_decode_step
+per step (plus commit) over a shuffled paged cache.
+
+``roofline`` is for each phase's dominant kernel, timed live with HIP events
+on the stream it runs on: the prefill gate_up GEMM (bound: MFMA) and the
+split-K decode attention (bound: HBM). ``cpu_baseline`` times the fp64 oracle
+on a bounded sample of the same prefill workload on the host cores.
+
+Inputs are seeded synthetic tensors generated on the device (weights
+N(0, 0.02^2), norm gains 1 + N(0, 0.02^2), activations and KV N(0, 1)).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode tok/s & HBM GB/s; prefill tok/s & MFMA util (8B-shaped layer)"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def randn(torch, gen, shape, std=1.0, mean=0.0):
+    t = torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32)
+    if std != 1.0:
+        t.mul_(std)
+    if mean != 0.0:
+        t.add_(mean)
+    return t.to(torch.bfloat16)
+
+
+def make_layer_weights(torch, B, shape, gen):
+    d, dq, dkv, f = shape.hidden, shape.d_q, shape.d_kv, shape.ffn
+    t = {
+        "attn_norm": randn(torch, gen, (d,), 0.02, 1.0),
+        "w_qkv": randn(torch, gen, (dq + 2 * dkv, d), 0.02),
+        "w_o": randn(torch, gen, (d, dq), 0.02),
+        "ffn_norm": randn(torch, gen, (d,), 0.02, 1.0),
+        "w_gate_up": randn(torch, gen, (2 * f, d), 0.02),  # iid rows: interleaving is a relabelling
+        "w_down": randn(torch, gen, (d, f), 0.02),
+    }
+    return t, B.layer_weights(**t)
+
+
+class EventTimer:
+    """Average duration of a launch sequence, HIP events on the current stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+
+    def __call__(self, fn, iters, warmup=2):
+        torch = self.torch
+        for _ in range(warmup):
+            fn()
+        s = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(iters):
+            fn()
+        e1.record(s)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / iters  # ms
+
+
+def bench_prefill(torch, B, A, wl, steps, warmup):
+    sh = wl.shape
+    gen = torch.Generator(device="cuda").manual_seed(1234)
+    cfg = B.make_cfg(sh)
+    tw, w = make_layer_weights(torch, B, sh, gen)
+    n, T = wl.prefill_seqs, wl.prefill_tokens
+    pages = (T + 15) // 16
+    pool = torch.empty(B.KV.pool_bytes(cfg, 1, n * pages + 8), dtype=torch.uint8, device="cuda")
+    kv = B.KV(cfg, 1, n * pages + 8, n, pages, pool, seed=0x5EED)
+    seqs = [kv.open() for _ in range(n)]
+    for s in seqs:
+        kv.alloc(s, T)
+    layer = B.Layer(cfg)
+    ws = torch.empty(B.Layer.workspace_bytes(cfg, n * T, n, pages), dtype=torch.uint8, device="cuda")
+    x = randn(torch, gen, (n * T, sh.hidden))
+    out = torch.empty_like(x)
+
+    def step():
+        layer.prefill(w, kv, 0, seqs, [T] * n, x, out, ws)
+        for s in seqs:  # positions restart at 0 each step (host-only metadata)
+            kv.truncate(s, 0)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    tokens = n * T
+
+    # dominant kernel: gate_up GEMM + SwiGLU epilogue, same launch path as the layer
+    M, N, K = tokens, 2 * sh.ffn, sh.hidden
+    hn = randn(torch, gen, (M, K))
+    m = torch.empty((M, sh.ffn), dtype=torch.bfloat16, device="cuda")
+    timer = EventTimer(torch)
+    g_ms = timer(lambda: B.op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_SWIGLU, M, N, K, hn, tw["w_gate_up"], None, m),
+                 iters=max(3, steps))
+    flops = 2.0 * M * N * K
+    gemm_tflops = flops / (g_ms * 1e-3) / 1e12
+    total_gemm = A.gemm_flops(tokens, sh.hidden, sh.d_q, sh.d_kv, sh.ffn)
+    attn = A.prefill_attention_flops([T] * n, sh.n_q, sh.head_dim)
+    res = {
+        "tok_s": tokens / (ms * 1e-3), "ms_per_step": ms,
+        "layer_tflops": (total_gemm + attn) / (ms * 1e-3) / 1e12,
+        "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K},
+        "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s", None).as_dict(),
+    }
+    del pool, ws, tw, x, out, hn, m
+    return res
+
+
+def bench_decode(torch, B, A, wl, steps, warmup):
+    from synth import gen as G
+    sh = wl.shape
+    gen = torch.Generator(device="cuda").manual_seed(4321)
+    cfg = B.make_cfg(sh)
+    tw, w = make_layer_weights(torch, B, sh, gen)
+    ctx = [int(c) for c in G.context_lengths(wl)]
+    nb = len(ctx)
+    extra = warmup + steps + 2
+    max_pages = (max(ctx) + extra + 15) // 16
+    n_pages = sum((c + extra + 15) // 16 for c in ctx) + 8
+    pool_elems = B.KV.pool_bytes(cfg, 1, n_pages) // 2
+    pool = randn(torch, gen, (pool_elems,))      # synthetic KV history, N(0, 1)
+    kv = B.KV(cfg, 1, n_pages, nb, max_pages, pool, seed=G.page_order_seed(wl))
+    seqs = [kv.open() for _ in range(nb)]
+    for s, c in zip(seqs, ctx):
+        kv.alloc(s, c + extra)
+        kv.commit([s], [c])
+    layer = B.Layer(cfg)
+    ws = torch.empty(B.Layer.workspace_bytes(cfg, nb, nb, max_pages), dtype=torch.uint8, device="cuda")
+    x = randn(torch, gen, (nb, sh.hidden))
+    out = torch.empty_like(x)
+
+    def step():
+        layer.decode_step(w, kv, 0, B.PS_PHASE_ANSWER, seqs, x, out, ws)
+        kv.commit(seqs, [1] * nb)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    lens0 = [kv.seq_len(s) for s in seqs]
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    # algorithmic bytes of the timed steps: KV read (len+1 keys) + weights
+    kv_bytes = sum(A.decode_attention_bytes([L + i + 1 for L in lens0], sh.n_kv, sh.head_dim, 2)
+                   for i in range(steps)) / steps
+    w_bytes = A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2)
+
+    # dominant kernel: split-K decode attention (+ its combine), same stream
+    q = randn(torch, gen, (nb, sh.n_q, sh.head_dim))
+    o = torch.empty((nb, sh.d_q), dtype=torch.bfloat16, device="cuda")
+    aws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    timer = EventTimer(torch)
+    a_ms = timer(lambda: B.op_decode_attention(kv, 0, seqs, q, o, aws), iters=max(10, steps))
+    lens = [kv.seq_len(s) for s in seqs]
+    a_bytes = A.decode_attention_bytes([L + 1 for L in lens], sh.n_kv, sh.head_dim, 2)
+    a_gbs = a_bytes / (a_ms * 1e-3) / 1e9
+    res = {
+        "tok_s": nb / (ms * 1e-3), "ms_per_step": ms, "batch": nb,
+        "ctx_mean": sum(ctx) / nb, "steps": steps,
+        "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
+        "step_bytes": kv_bytes + w_bytes,
+        "attention": {"us": a_ms * 1e3, "gbs": a_gbs, "bytes": a_bytes},
+        "roofline": A.Roofline("hbm", a_gbs, A.HBM_PEAK_GBS, "GB/s", None).as_dict(),
+    }
+    del pool, ws, tw, x, out, aws
+    return res
+
+
+def cpu_baseline(wl, n_tokens):
+    """The fp64 oracle on the host: one prompt's first n_tokens rows of the
+    prefill workload (weights regenerated by the seeded generator)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import layer as O
+    from synth import gen as G
+    w = {k: G.widen(v, "bf16") for k, v in G.layer_weights(wl, 0).items()}
+    x = G.widen(G.prefill_input(wl, n_tokens), "bf16")
+    t0 = time.perf_counter()
+    O.layer_sequence(w, wl.shape, x)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    del np
+    return {"value": n_tokens / dt, "unit": "tok/s", "cores": threads, "kind": "oracle",
+            "sample": f"1 prompt x first {n_tokens} tokens of the 8 x 2048 prefill, fp64 numpy, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=2048)
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_21719_amd import accounting as A
+    from paper_2608_21719_amd import binding as B
+    from synth.configs import CONFIGS
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    pre_wl = CONFIGS["llama8b_prefill"]
+    dec_wl = CONFIGS["llama8b_decode"]
+    log(f"prefill: {pre_wl.note}")
+    pre = bench_prefill(torch, B, A, pre_wl, a.steps, a.warmup)
+    log(f"prefill: {pre['tok_s']:.0f} tok/s, {pre['ms_per_step']:.3f} ms/step, gate_up {pre['gate_up_gemm']['tflops']:.0f} TFLOP/s")
+    torch.cuda.empty_cache()
+    dec = None
+    if not a.no_decode:
+        log(f"decode: {dec_wl.note}")
+        dec = bench_decode(torch, B, A, dec_wl, max(a.steps, 16), a.warmup)
+        log(f"decode: {dec['tok_s']:.0f} tok/s, {dec['ms_per_step'] * 1e3:.1f} us/step, "
+            f"attention {dec['attention']['gbs']:.0f} GB/s")
+    cpu = None
+    if not a.no_cpu_baseline:
+        log("cpu baseline: fp64 oracle on the host")
+        cpu = cpu_baseline(pre_wl, a.cpu_tokens)
+    line = {
+        "metric": METRIC, "value": pre["tok_s"], "unit": "tok/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": pre["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "8B-shaped layer prefill, 8 prompts x 2048 tokens (hidden 4096, 32 q / 8 kv "
+                               "heads, head_dim 128, SwiGLU 14336), bf16 weights/activations, fp32 accumulate",
+                   "global_batch": 8, "seq_len": 2048, "parallelism": "single GPU"},
+        "roofline": pre["roofline"],
+        "prefill": {k: v for k, v in pre.items() if k != "roofline"},
+        "decode": dec,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
