@@ -340,7 +340,7 @@ DecodePlan plan_decode(const std::vector<SeqInfo>& si, size_t first, int32_t spl
 std::vector<PrefillItem> plan_prefill(const std::vector<SeqInfo>& si, size_t count) {
   std::vector<PrefillItem> it;
   for (size_t b = 0; b < count; ++b)
-    for (int32_t q0 = 0; q0 < si[b].n_new; q0 += 64) it.push_back(PrefillItem{(int32_t)b, q0});
+    for (int32_t q0 = 0; q0 < si[b].n_new; q0 += fa_query_tile()) it.push_back(PrefillItem{(int32_t)b, q0});
   // most keys first (causal imbalance)
   std::stable_sort(it.begin(), it.end(), [&](const PrefillItem& a, const PrefillItem& c) {
     return si[a.b].kv_before + a.q_begin > si[c.b].kv_before + c.q_begin;
@@ -404,7 +404,7 @@ size_t meta_bound(const ps_layer_cfg& c, int32_t max_rows, int32_t max_seqs, int
   b += align_up(8ull * c.head_dim / 2, 256);
   const size_t parts = (size_t)max_seqs * ((max_pages + 7) / 8);
   b += align_up(sizeof(DecodeItem) * parts, 256) + 2 * align_up(4ull * max_seqs, 256);
-  b += align_up(sizeof(PrefillItem) * ((size_t)max_rows / 64 + max_seqs), 256);
+  b += align_up(sizeof(PrefillItem) * ((size_t)max_rows / 32 + max_seqs), 256);
   return b + 256;
 }
 

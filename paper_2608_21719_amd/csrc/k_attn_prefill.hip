@@ -25,14 +25,19 @@ namespace ps {
 
 namespace {
 constexpr int kHd = 128;
-constexpr int kQT = 64;              // query rows per workgroup
 constexpr int kKT = 32;              // keys per tile (two pages)
 constexpr int kKRow = kHd + 8;       // padded K row (elements)
 constexpr int kVRow = kKT + 8;       // padded V^T row (elements)
+constexpr int kPageCache = 2048;     // page ids cached in LDS (32768 positions)
+constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: lower register pressure, 2.3x faster than 2)
 }  // namespace
 
 // Four waves = four query heads of one KV group per workgroup; groups of 8
-// heads use two workgroups per KV head.
+// heads use two workgroups per KV head. K/V tiles are double-buffered: the
+// next tile's global loads are issued into registers before the current
+// tile's products, and written to the other LDS buffer after them, so one
+// barrier per tile suffices and load latency hides behind the MFMAs.
+template <int QB>  // 32-row query blocks per wave; the workgroup's query tile is 32 * QB rows
 __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
@@ -40,142 +45,198 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
                                                          const PrefillItem* __restrict__ items,
                                                          bf16_t* __restrict__ o, int n_kv, int G, float scale_log2) {
   constexpr int NT = 256;
-  __shared__ __attribute__((aligned(16))) bf16_t sK[kKT * kKRow];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[kHd * kVRow];
+  constexpr int kQT = 32 * QB;
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][kKT * kKRow];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][kHd * kVRow];
+  __shared__ int32_t sPage[kPageCache];  // the walk's page ids (first kPageCache pages)
 
   const int hq = G / 4;  // workgroups per KV head
   const int kvh = blockIdx.y / hq;
   const PrefillItem it = items[blockIdx.x];
   const SeqInfo s = si[it.b];
   const int n_q = n_kv * G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = threadIdx.x;
+  const int wave = t >> 6, lane = t & 63;
   const int g = lane >> 5, c = lane & 31;
   const int head = kvh * G + (blockIdx.y % hq) * 4 + wave;
   const int qn = min(kQT, s.n_new - it.q_begin);       // valid rows in this tile
   const int qpos0 = s.kv_before + it.q_begin;           // position of tile row 0
   const int n_keys = qpos0 + qn;                        // keys 0 .. last query position
+  const int kv_valid = s.kv_before + s.n_new;
   const int32_t* btr = bt + s.bt_off;
+  // every page a tile load can touch: keys below kv_valid inside the walk's
+  // n_tiles 32-key tiles (the last tile may reach past the last query)
+  const int n_tiles = (n_keys + kKT - 1) / kKT;
+  const int n_pages_walk = min((kv_valid + kPageTokens - 1) / kPageTokens, n_tiles * (kKT / kPageTokens));
+  for (int i = t; i < min(n_pages_walk, kPageCache); i += NT) sPage[i] = btr[i];
+  __syncthreads();
+  auto page_of = [&](int pg) { return pg < kPageCache ? sPage[pg] : btr[pg]; };
+  const long kvh_off = (long)kvh * (2L * kPageTokens * kHd);
+  const long page_stride = (long)n_kv * (2L * kPageTokens * kHd);
 
   // Q^T operand: lane (g, c) holds Q[row 32cb + c][16kk + 8g .. +8]
-  bf16x8_t qf[2][8];
+  bf16x8_t qf[QB][8];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < QB; ++cb) {
     int r = min(32 * cb + c, qn - 1);
     const bf16_t* qp = q + ((long)(s.row_start + it.q_begin + r) * n_q + head) * kHd + 8 * g;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) qf[cb][kk] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * kk));
   }
 
-  f32x16_t oacc[2][4];
+  f32x16_t oacc[QB][4];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
+  for (int cb = 0; cb < QB; ++cb)
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[cb][db][r] = 0.f;
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+  float m[QB], l[QB];
+#pragma unroll
+  for (int cb = 0; cb < QB; ++cb) {
+    m[cb] = -INFINITY;
+    l[cb] = 0.f;
+  }
 
-  const int n_tiles = (n_keys + kKT - 1) / kKT;
-  const int kv_valid = s.kv_before + s.n_new;
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int k0 = kt * kKT;
-    // ---- stage K [32][128] and V^T [128][32] (keys permuted per page as
-    // 0-3, 8-11, 4-7, 12-15) into LDS
-    for (int e = threadIdx.x; e < kKT * (kHd / 8); e += NT) {
+  // staging assignment: K chunks (key, 16-byte chunk) e = t, t + 256;
+  // V^T halves (page in tile, dim, half) e = t, t + 256
+  uint4 rk[2], rv[2];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = t + i * NT;
       const int key = e >> 4, ch = e & 15;
-      const int pg = (k0 + key) / kPageTokens;
-      uint4 w = make_uint4(0, 0, 0, 0);
-      if (k0 + key < kv_valid) {
-        const bf16_t* src = pool + ((long)btr[pg] * n_kv + kvh) * (2L * kPageTokens * kHd) +
-                            (long)((k0 + key) % kPageTokens) * kHd + ch * 8;
-        w = *(const uint4*)src;
-      }
-      *(uint4*)(sK + key * kKRow + ch * 8) = w;
-    }
-    for (int e = threadIdx.x; e < 2 * kHd * 2; e += NT) {
-      // (page in tile, dim, 16-byte half of its 16-key row)
+      const int kpos = k0 + key;
+      rk[i] = make_uint4(0, 0, 0, 0);
+      if (kpos < kv_valid)
+        rk[i] = *(const uint4*)(pool + page_of(kpos / kPageTokens) * page_stride + kvh_off +
+                                (long)(kpos % kPageTokens) * kHd + ch * 8);
       const int pt = e / (kHd * 2), rem = e - pt * (kHd * 2);
       const int dim = rem >> 1, hf = rem & 1;
-      const int pfirst = k0 + pt * kPageTokens;  // first key of this page
-      uint4 w = make_uint4(0, 0, 0, 0);
+      const int pfirst = k0 + pt * kPageTokens;
+      rv[i] = make_uint4(0, 0, 0, 0);
       if (pfirst < kv_valid) {
-        const bf16_t* src = pool + ((long)btr[pfirst / kPageTokens] * n_kv + kvh) * (2L * kPageTokens * kHd) +
-                            (long)kPageTokens * kHd + (long)dim * kPageTokens + hf * 8;
-        w = *(const uint4*)src;
-        // zero values of keys beyond the written length (stale memory)
-        const int valid = kv_valid - pfirst - hf * 8;  // keys valid in this half
+        uint4 w = *(const uint4*)(pool + page_of(pfirst / kPageTokens) * page_stride + kvh_off +
+                                  (long)kPageTokens * kHd + (long)dim * kPageTokens + hf * 8);
+        const int valid = kv_valid - pfirst - hf * 8;  // zero keys past the written length
         if (valid < 8) {
           uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-          for (int i = 0; i < 8; ++i)
-            if (i >= valid) ws[i >> 1] &= (i & 1) ? 0x0000ffffu : 0xffff0000u;
+          for (int j = 0; j < 8; ++j)
+            if (j >= valid) ws[j >> 1] &= (j & 1) ? 0x0000ffffu : 0xffff0000u;
           w = make_uint4(ws[0], ws[1], ws[2], ws[3]);
         }
+        rv[i] = w;
       }
-      // half hf holds keys 8hf..8hf+7 = (8hf..+3, 8hf+4..+7); stored order
-      // per page is [0-3][8-11][4-7][12-15] (8-byte groups)
-      bf16_t* dst = sV + dim * kVRow + pt * kPageTokens;
-      *(uint2*)(dst + hf * 4) = make_uint2(w.x, w.y);      // keys 8hf+0..3 -> group hf
-      *(uint2*)(dst + 8 + hf * 4) = make_uint2(w.z, w.w);  // keys 8hf+4..7 -> group 2+hf
     }
-    __syncthreads();
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = t + i * NT;
+      const int key = e >> 4, ch = e & 15;
+      *(uint4*)(&sK[buf][key * kKRow + ch * 8]) = rk[i];
+      const int pt = e / (kHd * 2), rem = e - pt * (kHd * 2);
+      const int dim = rem >> 1, hf = rem & 1;
+      // half hf = keys 8hf..8hf+7; stored per page as [0-3][8-11][4-7][12-15]
+      bf16_t* dst = &sV[buf][dim * kVRow + pt * kPageTokens];
+      *(uint2*)(dst + hf * 4) = make_uint2(rv[i].x, rv[i].y);
+      *(uint2*)(dst + 8 + hf * 4) = make_uint2(rv[i].z, rv[i].w);
+    }
+  };
 
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int k0 = kt * kKT;
+    const int buf = kt & 1;
+    if (kt + 1 < n_tiles) gload(k0 + kKT);
+    const bf16_t* K = sK[buf];
+    const bf16_t* V = sV[buf];
+    // S^T for all row blocks, each K fragment read once
+    bool act[QB];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      if (32 * cb >= qn) break;
-      f32x16_t sacc;
+    for (int cb = 0; cb < QB; ++cb) act[cb] = 32 * cb < qn;
+    f32x16_t sacc[QB];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+    for (int cb = 0; cb < QB; ++cb)
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK + c * kKRow + 16 * kk + 8 * g));
-        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[cb][kk], sacc, 0, 0, 0);
-      }
-      // sacc[r] = score(key 8(r/4) + 4g + r%4, query c)
+      for (int r = 0; r < 16; ++r) sacc[cb][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(K + c * kKRow + 16 * kk + 8 * g));
+#pragma unroll
+      for (int cb = 0; cb < QB; ++cb)
+        if (act[cb]) sacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[cb][kk], sacc[cb], 0, 0, 0);
+    }
+    // sacc[cb][r] = score(key 8(r/4) + 4g + r%4, query 32cb + c); mask only
+    // on tiles that reach past the block's first query position
+    uint32_t pk[QB][8];
+#pragma unroll
+    for (int cb = 0; cb < QB; ++cb) {
+      if (!act[cb]) continue;
       const int qpos = qpos0 + 32 * cb + c;
       float mx = -INFINITY;
+      if (k0 + kKT - 1 <= qpos0 + 32 * cb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + 8 * (r >> 2) + 4 * g + (r & 3);
-        sacc[r] = (key <= qpos) ? sacc[r] * scale_log2 : -INFINITY;
-        mx = fmaxf(mx, sacc[r]);
+        for (int r = 0; r < 16; ++r) {
+          sacc[cb][r] *= scale_log2;
+          mx = fmaxf(mx, sacc[cb][r]);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 8 * (r >> 2) + 4 * g + (r & 3);
+          sacc[cb][r] = (key <= qpos) ? sacc[cb][r] * scale_log2 : -INFINITY;
+          mx = fmaxf(mx, sacc[cb][r]);
+        }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m[cb], mx);
-      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m[cb] - m_new);
-      uint32_t pk[8];
+      const float m_new = fmaxf(m[cb], mx);  // finite: key 0 is in tile 0
       float psum = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        float p0 = (m_new == -INFINITY) ? 0.f : exp2f(sacc[2 * i] - m_new);
-        float p1 = (m_new == -INFINITY) ? 0.f : exp2f(sacc[2 * i + 1] - m_new);
-        pk[i] = pack_bf2(p0, p1);
-        psum += bf_lo(pk[i]) + bf_hi(pk[i]);
+        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(sacc[cb][2 * i] - m_new),
+                             __builtin_amdgcn_exp2f(sacc[cb][2 * i + 1] - m_new));
+        psum += bf_lo(pk[cb][i]) + bf_hi(pk[cb][i]);
       }
-      l[cb] = l[cb] * alpha + psum;
+      // rescale only if some row's running max moved (lane-local factor)
+      if (__any(m_new != m[cb])) {
+        const float alpha = __builtin_amdgcn_exp2f(m[cb] - m_new);
+        l[cb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[cb][db][r] *= alpha;
+      }
+      l[cb] += psum;
       m[cb] = m_new;
+    }
+    // O^T += V^T P^T for all row blocks, each V fragment read once
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
+    for (int kk2 = 0; kk2 < 2; ++kk2) {
+      bf16x8_t bp[QB];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[cb][db][r] *= alpha;
+      for (int cb = 0; cb < QB; ++cb)
+        bp[cb] = __builtin_bit_cast(
+            bf16x8_t, make_uint4(pk[cb][4 * kk2], pk[cb][4 * kk2 + 1], pk[cb][4 * kk2 + 2], pk[cb][4 * kk2 + 3]));
 #pragma unroll
-      for (int kk2 = 0; kk2 < 2; ++kk2) {
-        const bf16x8_t bp =
-            __builtin_bit_cast(bf16x8_t, make_uint4(pk[4 * kk2], pk[4 * kk2 + 1], pk[4 * kk2 + 2], pk[4 * kk2 + 3]));
+      for (int db = 0; db < 4; ++db) {
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, *(const uint4*)(V + (32 * db + c) * kVRow + kk2 * kPageTokens + 8 * g));
 #pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          bf16x8_t a = __builtin_bit_cast(
-              bf16x8_t, *(const uint4*)(sV + (32 * db + c) * kVRow + kk2 * kPageTokens + 8 * g));
-          oacc[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp, oacc[cb][db], 0, 0, 0);
-        }
+        for (int cb = 0; cb < QB; ++cb)
+          if (act[cb]) oacc[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp[cb], oacc[cb][db], 0, 0, 0);
       }
     }
+    if (kt + 1 < n_tiles) lstore(buf ^ 1);
     __syncthreads();
   }
 
   // ---- normalise and store: lane holds query c, dims 32db + 8(r/4) + 4g + r%4
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < QB; ++cb) {
     const int r0 = 32 * cb + c;
     if (r0 >= qn) continue;
     const float L = l[cb] + __shfl_xor(l[cb], 32);
@@ -193,14 +254,22 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
   }
 }
 
-int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
-                      const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st) {
+int fa_query_tile() { return 32 * kFaQB; }
+
+template <int QB>
+int launch_fa_prefill_qb(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
+                         const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st) {
   if (n_items == 0) return 0;
   if (G % 4 != 0) return -1;
   dim3 grid(n_items, n_kv * (G / 4));
-  hipLaunchKernelGGL(fa_prefill_kernel, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt,
-                     items, (bf16_t*)o, n_kv, G, scale_log2);
+  hipLaunchKernelGGL(fa_prefill_kernel<QB>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si,
+                     bt, items, (bf16_t*)o, n_kv, G, scale_log2);
   return 0;
+}
+
+int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
+                      const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st) {
+  return launch_fa_prefill_qb<kFaQB>(G, n_items, n_kv, q, pool_layer, si, bt, items, o, scale_log2, st);
 }
 
 }  // namespace ps

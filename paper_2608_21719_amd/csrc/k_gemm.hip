@@ -1,9 +1,10 @@
 // GEMMs of the layer: C = epilogue(A W^T), A [M, K], W [N, K] (both
 // K-contiguous, the nn.Linear layout), fp32 accumulation (gfx950).
 //
-//  * gemm_tile_kernel: prefill-sized M. 256x256x64 workgroup tile, four waves
-//    of 128x128, v_mfma_f32_32x32x16_bf16, operands staged through
-//    double-buffered, XOR-swizzled LDS (128 KiB). MFMA-bound.
+//  * gemm_tile_kernel: prefill-sized M. 256x256x64 workgroup tile, eight
+//    waves of 128x64 (two per SIMD), v_mfma_f32_32x32x16_bf16, operands
+//    staged through double-buffered, XOR-swizzled LDS (128 KiB) by direct
+//    global->LDS loads. MFMA-bound.
 //  * gemm_skinny_kernel: decode-sized M (<= 64). Streams W once from HBM
 //    with 16-byte loads, one 16-column MFMA block per wave, activations
 //    staged in LDS and shared by the workgroup's four waves; K may be split
@@ -28,26 +29,56 @@ template <> __device__ __forceinline__ void st_elt<float>(float* p, long i, floa
 template <> __device__ __forceinline__ void st_elt<bf16_t>(bf16_t* p, long i, float v) { p[i] = f2bf(v); }
 
 // ====================================================================== tile
-namespace tile {
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 256;                 // threads
-constexpr int WTM = 128, WTN = 128;     // wave tile
-constexpr int FM = WTM / 32, FN = WTN / 32;
-constexpr int TILE_ELTS = BM * BK;      // per operand per stage
-constexpr int LOADS = TILE_ELTS / 8 / NT;  // 16-byte loads per lane per operand per stage (8)
+// Workgroup tile BM x BN, K step BK, WAVES_M x WAVES_N waves, STAGES-deep
+// ring of LDS buffers filled by direct global->LDS loads
+// (global_load_lds_dwordx4): one wave instruction fills 1 KiB of LDS, lane l
+// landing at +16 l. LDS rows hold BK bf16 (BK/8 16-byte chunks), XOR-
+// swizzled so that the 16-byte operand reads of 16 consecutive rows hit 16
+// distinct 16-byte bank groups; the global address of each lane is chosen
+// so that the linear fill lands in swizzled order.
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_>
+struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
+  static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+  static constexpr int NW = WAVES_M * WAVES_N;
+  static constexpr int NT = 64 * NW;
+  static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  static constexpr int FM = WTM / 32, FN = WTN / 32;
+  static constexpr int CPR = BK / 8;               // 16-byte chunks per LDS row
+  static constexpr int ROWS_PER_LOAD = 64 / CPR;   // rows one wave instruction fills
+  static constexpr int A_ELTS = BM * BK, B_ELTS = BN * BK;
+  static constexpr int STAGE_ELTS = A_ELTS + B_ELTS;
+  static constexpr int A_LOADS = BM / ROWS_PER_LOAD / NW;  // per wave per stage
+  static constexpr int B_LOADS = BN / ROWS_PER_LOAD / NW;
+  static constexpr int LOADS = A_LOADS + B_LOADS;
+  static constexpr size_t LDS_BYTES = (size_t)STAGES * STAGE_ELTS * 2;
+  static_assert(FM >= 1 && FN >= 1 && A_LOADS >= 1 && B_LOADS >= 1, "tile shape");
+  static_assert(BM % (ROWS_PER_LOAD * NW) == 0 && BN % (ROWS_PER_LOAD * NW) == 0, "load split");
+  __device__ static int swz(int row, int ch) {
+    return row * BK + ((ch ^ ((row / (16 / CPR)) % CPR)) << 3);
+  }
+};
 
-// element offset of (row, 16-byte chunk ch) in a swizzled [rows][64] tile
-__device__ __forceinline__ int swz(int row, int ch) { return row * BK + ((ch ^ ((row >> 1) & 7)) << 3); }
-}  // namespace tile
+// One 16-byte global->LDS fill per lane (global_load_lds_dwordx4). Kept in
+// a non-template device function: used directly inside a kernel template
+// the builtin makes the host pass drop the kernel's instantiation.
+__device__ __forceinline__ void load_lds16(const bf16_t* g, bf16_t* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
 
-template <int EPI, typename TR, typename TC>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_tile_kernel(
+// s_waitcnt with only vmcnt = n (n < 64), other counters not waited on
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <class CF, int EPI, typename TR, typename TC>
+__global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, const TR* __restrict__ R, TC* __restrict__ C,
     int M, int N, int K, int tiles_n) {
-  using namespace tile;
+  constexpr int BM = CF::BM, BN = CF::BN, BK = CF::BK, STAGES = CF::STAGES;
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-  bf16_t* sA = smem;                      // [2][BM*BK]
-  bf16_t* sB = smem + 2 * TILE_ELTS;      // [2][BN*BK]
 
   // XCD-aware tile order: consecutive workgroup ids go round-robin over the
   // 8 XCDs; give each XCD a contiguous range of tiles so that tiles sharing
@@ -67,78 +98,83 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / CF::WAVES_N, wn = wave % CF::WAVES_N;
   const int g = lane >> 5, c = lane & 31;
 
-  // Direct global->LDS loads (global_load_lds_dwordx4): one instruction of
-  // a wave fills 1 KiB of LDS, lane l landing at +16*l, i.e. 8 rows of the
-  // [rows][64] tile. Lane l therefore fetches the logical chunk that the
-  // swizzle stores at its LDS position: row r = 8*i + l/8, position l%8,
-  // chunk (l%8) ^ ((r >> 1) & 7). Wave w fills rows [64w, 64w + 64).
-  const int lrow = lane >> 3, lpos = lane & 7;
-  const bf16_t* ga[LOADS];
-  const bf16_t* gb[LOADS];
+  // per-lane global sources of this wave's loads (row block of the wave)
+  const int lrow = lane / CF::CPR, lpos = lane % CF::CPR;
+  const bf16_t* ga[CF::A_LOADS];
+  const bf16_t* gb[CF::B_LOADS];
 #pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const int row = wave * 64 + i * 8 + lrow;
-    const int ch = lpos ^ ((row >> 1) & 7);
+  for (int i = 0; i < CF::A_LOADS; ++i) {
+    const int row = (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD + lrow;
+    const int ch = lpos ^ ((row / (16 / CF::CPR)) % CF::CPR);
     ga[i] = A + (long)min(m0 + row, M - 1) * K + ch * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < CF::B_LOADS; ++i) {
+    const int row = (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD + lrow;
+    const int ch = lpos ^ ((row / (16 / CF::CPR)) % CF::CPR);
     gb[i] = W + (long)(n0 + row) * K + ch * 8;
   }
-  auto gload = [&](int k0, int buf) {
-    bf16_t* a = sA + buf * TILE_ELTS + wave * 64 * BK;
-    bf16_t* b = sB + buf * TILE_ELTS + wave * 64 * BK;
+  auto gload = [&](int k0, int stage) {
+    bf16_t* a = smem + stage * CF::STAGE_ELTS;
+    bf16_t* b = a + CF::A_ELTS;
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      __builtin_amdgcn_global_load_lds(ga[i] + k0, (__attribute__((address_space(3))) void*)(a + i * 8 * BK), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(gb[i] + k0, (__attribute__((address_space(3))) void*)(b + i * 8 * BK), 16, 0, 0);
-    }
+    for (int i = 0; i < CF::A_LOADS; ++i)
+      load_lds16(ga[i] + k0, a + (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD * BK);
+#pragma unroll
+    for (int i = 0; i < CF::B_LOADS; ++i)
+      load_lds16(gb[i] + k0, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
   };
 
-  f32x16_t acc[FM][FN];
+  f32x16_t acc[CF::FM][CF::FN];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < CF::FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+    for (int j = 0; j < CF::FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int KT = K / BK;
-  gload(0, 0);
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's LDS fills landed
-  __syncthreads();
+  // prologue: stages 0 .. STAGES-2 in flight
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < KT) gload(st * BK, st);
   for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * BK, buf ^ 1);
-    const bf16_t* a = sA + buf * TILE_ELTS;
-    const bf16_t* b = sB + buf * TILE_ELTS;
+    // stage kt has landed once at most (STAGES-2) later stages are pending
+    if (kt + STAGES - 2 < KT) wait_vmcnt<(STAGES - 2) * CF::LOADS>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    // refill the slot consumed in iteration kt-1
+    if (kt + STAGES - 1 < KT) gload((kt + STAGES - 1) * BK, (kt + STAGES - 1) % STAGES);
+    const bf16_t* a = smem + (kt % STAGES) * CF::STAGE_ELTS;
+    const bf16_t* b = a + CF::A_ELTS;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8_t af[FM], bfr[FN];
+      bf16x8_t af[CF::FM], bfr[CF::FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + swz(wm * WTM + i * 32 + c, 2 * kk + g)));
+      for (int i = 0; i < CF::FM; ++i)
+        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 32 + c, 2 * kk + g)));
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + swz(wn * WTN + j * 32 + c, 2 * kk + g)));
+      for (int j = 0; j < CF::FN; ++j)
+        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 32 + c, 2 * kk + g)));
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < CF::FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int j = 0; j < CF::FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
   }
 
   // epilogue: acc[i][j][r] = C[row 8(r/4) + 4g + r%4][col c] of block (i, j)
-  const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN;
+  const int rbase = m0 + wm * CF::WTM, cbase = n0 + wn * CF::WTN;
   if constexpr (EPI == 2) {
     const int ldc = N / 2;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < CF::FM; ++i)
 #pragma unroll
-      for (int jp = 0; jp < FN / 2; ++jp)
+      for (int jp = 0; jp < CF::FN / 2; ++jp)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = rbase + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
@@ -149,9 +185,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
   } else {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < CF::FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < CF::FN; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = rbase + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
@@ -358,17 +394,25 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }
 
 // ==================================================================== launch
-template <int EPI, typename TR, typename TC>
-static int launch_tile(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
-  using namespace tile;
+// Default prefill tile configuration.
+using TileDefault = TileCfg<256, 256, 64, 2, 4, 2>;  // 8 waves of 128x64, 2 per SIMD
+
+template <class CF, int EPI, typename TR, typename TC>
+int launch_tile_cfg(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
+  constexpr int BM = CF::BM, BN = CF::BN;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-  const size_t lds = 4 * TILE_ELTS * sizeof(bf16_t);
-  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<EPI, TR, TC>,
-                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<CF, EPI, TR, TC>,
+                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                      (int)CF::LDS_BYTES);
   if (attr != hipSuccess) return -1;
-  hipLaunchKernelGGL((gemm_tile_kernel<EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(NT), lds, st,
+  hipLaunchKernelGGL((gemm_tile_kernel<CF, EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(CF::NT), CF::LDS_BYTES, st,
                      (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n);
   return 0;
+}
+
+template <int EPI, typename TR, typename TC>
+static int launch_tile(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
+  return launch_tile_cfg<TileDefault, EPI, TR, TC>(M, N, K, A, W, R, C, st);
 }
 
 template <int EPI, typename TR, typename TC>
@@ -456,7 +500,7 @@ int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, con
 #undef RED_CASE
     return -1;
   }
-  if (N % tile::BN != 0) return -1;
+  if (N % 256 != 0) return -1;
 #define TILE_CASE(E, TR_, TC_, rd, cd) \
   if (epi == E && r_dt == rd && c_dt == cd) return launch_tile<E, TR_, TC_>(M, N, K, A, W, R, C, st);
   TILE_CASE(0, float, bf16_t, 0, 1)
@@ -484,6 +528,6 @@ int gemm_check(int dtype, int epi, int M, int N, int K) {
   if (dtype == 0) return 0;
   if (dtype != 1 || K % 64 != 0) return -1;
   if (M <= skinny::MAXM && N % skinny::BN == 0 && K % skinny::KCH == 0) return 0;
-  return (N % tile::BN == 0) ? 0 : -1;
+  return (N % 256 == 0) ? 0 : -1;
 }
 }  // namespace ps

@@ -28,6 +28,7 @@ int launch_decode_attn(int G, int n_items, int n_kv, int n_seqs, const void* q, 
 int launch_attn_generic(int dt, int row0, int rows, int n_seqs, int n_q, int n_kv, int hd, const void* q,
                         const void* pool_layer, const SeqInfo* si, const int32_t* bt, void* o, float scale,
                         hipStream_t st);
+int fa_query_tile();  // query rows per prefill work item
 int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
                       const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st);
 
