@@ -189,23 +189,98 @@ def bench_decode(torch, B, A, wl, steps, warmup):
     return res
 
 
-def cpu_baseline(wl, n_tokens):
-    """The fp64 oracle on the host: one prompt's first n_tokens rows of the
-    prefill workload (weights regenerated by the seeded generator)."""
-    import numpy as np
+def bench_think(torch, B, A, wl, steps, warmup):
+    """Reasoning think phase: decode B=32 over long log-normal contexts, plus
+    one mixed step fusing 4 new 512-token prefill chunks with the 32 decodes."""
+    from synth import gen as G
+    sh = wl.shape
+    gen = torch.Generator(device="cuda").manual_seed(777)
+    cfg = B.make_cfg(sh)
+    tw, w = make_layer_weights(torch, B, sh, gen)
+    ctx = [int(c) for c in G.context_lengths(wl)]
+    nb, nc, chunk = len(ctx), wl.mixed_new, wl.mixed_chunk
+    extra = warmup + steps + 4
+    max_pages = (max(max(ctx) + extra, chunk) + 15) // 16
+    n_pages = sum((c + extra + 15) // 16 for c in ctx) + nc * ((chunk + 15) // 16) + 8
+    pool = randn(torch, gen, (B.KV.pool_bytes(cfg, 1, n_pages) // 2,))
+    kv = B.KV(cfg, 1, n_pages, nb + nc, max_pages, pool, seed=G.page_order_seed(wl))
+    seqs = [kv.open() for _ in range(nb)]
+    for s, c in zip(seqs, ctx):
+        kv.alloc(s, c + extra)
+        kv.commit([s], [c])
+    layer = B.Layer(cfg)
+    ws = torch.empty(B.Layer.workspace_bytes(cfg, nc * chunk + nb, nb + nc, max_pages), dtype=torch.uint8,
+                     device="cuda")
+    x = randn(torch, gen, (nb, sh.hidden))
+    out = torch.empty_like(x)
+
+    def step():
+        layer.decode_step(w, kv, 0, B.PS_PHASE_THINK, seqs, x, out, ws)
+        kv.commit(seqs, [1] * nb)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    lens0 = [kv.seq_len(s) for s in seqs]
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    kv_bytes = sum(A.decode_attention_bytes([L + i + 1 for L in lens0], sh.n_kv, sh.head_dim, 2)
+                   for i in range(steps)) / steps
+    w_bytes = A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2)
+    q = randn(torch, gen, (nb, sh.n_q, sh.head_dim))
+    o = torch.empty((nb, sh.d_q), dtype=torch.bfloat16, device="cuda")
+    timer = EventTimer(torch)
+    a_ms = timer(lambda: B.op_decode_attention(kv, 0, seqs, q, o, ws), iters=max(10, steps))
+    a_bytes = A.decode_attention_bytes([kv.seq_len(s) + 1 for s in seqs], sh.n_kv, sh.head_dim, 2)
+
+    # mixed step: chunk rows first, then one row per decoding sequence
+    new = [kv.open() for _ in range(nc)]
+    for s in new:
+        kv.alloc(s, chunk)
+    xm = randn(torch, gen, (nc * chunk + nb, sh.hidden))
+    om = torch.empty_like(xm)
+
+    def mixed():
+        layer.mixed_step(w, kv, 0, new, [chunk] * nc, seqs, xm, om, ws)
+
+    m_ms = timer(mixed, iters=max(5, steps // 2))
+    rows = nc * chunk + nb
+    m_flops = A.gemm_flops(rows, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) + \
+        A.prefill_attention_flops([chunk] * nc, sh.n_q, sh.head_dim)
+    res = {
+        "tok_s": nb / (ms * 1e-3), "ms_per_step": ms, "batch": nb, "ctx_mean": sum(ctx) / nb,
+        "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
+        "attention": {"us": a_ms * 1e3, "gbs": a_bytes / (a_ms * 1e-3) / 1e9, "bytes": a_bytes},
+        "mixed_step": {"ms": m_ms, "rows": rows, "tok_s": rows / (m_ms * 1e-3),
+                       "tflops": m_flops / (m_ms * 1e-3) / 1e12},
+    }
+    del pool, ws, tw, x, out, xm, om
+    return res
+
+
+def cpu_baseline(wl, n_tokens, budget_s=10.0):
+    """The fp64 oracle on the host over whole prompts of the prefill workload
+    (weights regenerated by the seeded generator), prompt after prompt until
+    about budget_s seconds of oracle time or all prompts are done."""
     from threadpoolctl import threadpool_info
 
     from oracle import layer as O
     from synth import gen as G
     w = {k: G.widen(v, "bf16") for k, v in G.layer_weights(wl, 0).items()}
-    x = G.widen(G.prefill_input(wl, n_tokens), "bf16")
-    t0 = time.perf_counter()
-    O.layer_sequence(w, wl.shape, x)
-    dt = time.perf_counter() - t0
+    x = G.widen(G.prefill_input(wl, wl.prefill_seqs * n_tokens), "bf16")
+    done, dt = 0, 0.0
+    while done < wl.prefill_seqs and dt < budget_s:
+        t0 = time.perf_counter()
+        O.layer_sequence(w, wl.shape, x[done * n_tokens:(done + 1) * n_tokens])
+        dt += time.perf_counter() - t0
+        done += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    del np
-    return {"value": n_tokens / dt, "unit": "tok/s", "cores": threads, "kind": "oracle",
-            "sample": f"1 prompt x first {n_tokens} tokens of the 8 x 2048 prefill, fp64 numpy, {dt:.1f} s"}
+    return {"value": done * n_tokens / dt, "unit": "tok/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of the {wl.prefill_seqs} prompts x {n_tokens} tokens of the prefill workload, "
+                      f"fp64 numpy, {dt:.1f} s"}
 
 
 def main():
@@ -244,6 +319,14 @@ def main():
         dec = bench_decode(torch, B, A, dec_wl, max(a.steps, 16), a.warmup)
         log(f"decode: {dec['tok_s']:.0f} tok/s, {dec['ms_per_step'] * 1e3:.1f} us/step, "
             f"attention {dec['attention']['gbs']:.0f} GB/s")
+    think = None
+    if not a.no_decode:
+        th_wl = CONFIGS["llama8b_think"]
+        log(f"think: {th_wl.note}")
+        think = bench_think(torch, B, A, th_wl, max(a.steps, 16), a.warmup)
+        log(f"think: {think['tok_s']:.0f} tok/s, attention {think['attention']['gbs']:.0f} GB/s, "
+            f"mixed step {think['mixed_step']['ms']:.3f} ms")
+        torch.cuda.empty_cache()
     cpu = None
     if not a.no_cpu_baseline:
         log("cpu baseline: fp64 oracle on the host")
@@ -258,6 +341,7 @@ def main():
         "roofline": pre["roofline"],
         "prefill": {k: v for k, v in pre.items() if k != "roofline"},
         "decode": dec,
+        "think": think,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

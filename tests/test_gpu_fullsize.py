@@ -1,0 +1,134 @@
+"""Parity at the benchmarked sizes, on sampled outputs (GPU).
+
+The layer runs exactly as bench.py times it (8 x 2048 prefill; decode batch 64
+over U{1024..4096} contexts; think decode batch 32 over log-normal contexts
+up to 32k plus the fused mixed step). The fp64 oracle then evaluates a sample
+of sequences in full (every row of a sampled prefill sequence; the decode row
+of sampled decode sequences over their whole history) and the outputs are
+compared with the end-to-end normwise bound. Synthetic KV history is drawn by
+a seeded torch generator, copied to the host by torch, and written with
+ps_kv_append: the oracle's inputs never pass through the library's kernels.
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as O
+from synth import gen
+from synth.configs import CONFIGS
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_21719_amd import binding as B  # noqa: E402
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(scope="module")
+def layer8b():
+    wl = CONFIGS["llama8b_prefill"]
+    w = gen.layer_weights(wl, 0)
+    return {"wl": wl, "wf": H.weights_f64(w, "bf16"), "dev": H.DeviceLayer(w, "bf16")}
+
+
+def normwise_ok(got, ref, what):
+    mx, rms = H.normwise(got, ref)
+    assert mx <= H.NORMWISE_TOL and rms <= H.NORMWISE_TOL, f"{what}: normwise max {mx:.2e} rms {rms:.2e}"
+
+
+def test_prefill_8x2048_sampled_sequences(layer8b):
+    wl, sh = layer8b["wl"], layer8b["wl"].shape
+    n, T = wl.prefill_seqs, wl.prefill_tokens
+    pool = H.Pool(sh, n * T // 16 + 8, n, T // 16, seed=gen.page_order_seed(wl))
+    layer = B.Layer(pool.cfg)
+    seqs = [pool.kv.open() for _ in range(n)]
+    for s in seqs:
+        pool.kv.alloc(s, T)
+    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, n * T, n, T // 16))
+    x = gen.prefill_input(wl, n * T)
+    out = H.empty((n * T, sh.hidden), "bf16")
+    layer.prefill(layer8b["dev"].w, pool.kv, 0, seqs, [T] * n, H.to_dev(x, "bf16"), out, ws)
+    sync()
+    got = H.to_f64(out)
+    xf = gen.widen(x, "bf16")
+    for b in (0, n - 1):
+        ref = O.layer_sequence(layer8b["wf"], sh, xf[b * T:(b + 1) * T])["out"]
+        normwise_ok(got[b * T:(b + 1) * T], ref, f"prefill seq {b}")
+        # and the first and last rows on their own
+        normwise_ok(got[b * T], ref[0], f"seq {b} row 0")
+        normwise_ok(got[(b + 1) * T - 1], ref[-1], f"seq {b} row {T - 1}")
+
+
+def _decode_fullsize(layer8b, wl, sample, phase, mixed=False):
+    sh = wl.shape
+    ctx = [int(c) for c in gen.context_lengths(wl)]
+    nb = len(ctx)
+    chunk, nc = wl.mixed_chunk, wl.mixed_new
+    max_pages = (max(max(ctx) + 1, chunk) + 15) // 16
+    n_pages = sum((c + 16) // 16 for c in ctx) + nc * ((chunk + 15) // 16) + 8
+    pool = H.Pool(sh, n_pages, nb + nc, max_pages, seed=gen.page_order_seed(wl))
+    kv = pool.kv
+    layer = B.Layer(pool.cfg)
+    rows = nb + (nc * chunk if mixed else 0)
+    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, max(rows, 64), nb + nc, max_pages))
+    g = torch.Generator(device="cuda").manual_seed(wl.cfg_id * 1000 + 7)
+    seqs = [kv.open() for _ in range(nb)]
+    hist = {}
+    for b, (s, c) in enumerate(zip(seqs, ctx)):
+        kv.alloc(s, c + 1)
+        k = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        kv.append(0, [s], [c], k, v, ws)
+        kv.commit([s], [c])
+        if b in sample:
+            hist[b] = (H.to_f64(k), H.to_f64(v))
+        del k, v
+    sync()
+    xd = gen.decode_input(wl, nb, 0)
+    new = []
+    if mixed:
+        new = [kv.open() for _ in range(nc)]
+        for s in new:
+            kv.alloc(s, chunk)
+        xc = gen.mixed_input(wl, nc * chunk)
+        x = np.concatenate([xc, xd])
+        out = H.empty((rows, sh.hidden), "bf16")
+        layer.mixed_step(layer8b["dev"].w, kv, 0, new, [chunk] * nc, seqs, H.to_dev(x, "bf16"), out, ws)
+    else:
+        x = xd
+        out = H.empty((nb, sh.hidden), "bf16")
+        layer.decode_step(layer8b["dev"].w, kv, 0, phase, seqs, H.to_dev(x, "bf16"), out, ws)
+    sync()
+    got = H.to_f64(out)
+    xf = gen.widen(x, "bf16")
+    off = nc * chunk if mixed else 0
+    for b in sample:
+        ref = O.layer_sequence(layer8b["wf"], sh, xf[off + b:off + b + 1], *hist[b])["out"][0]
+        normwise_ok(got[off + b], ref, f"decode seq {b} ctx {ctx[b]}")
+    if mixed:
+        for i in (0, nc - 1):
+            ref = O.layer_sequence(layer8b["wf"], sh, xf[i * chunk:(i + 1) * chunk])["out"]
+            normwise_ok(got[i * chunk:(i + 1) * chunk], ref, f"mixed chunk {i}")
+    return ctx
+
+
+def test_decode_batch64_sampled_sequences(layer8b):
+    ctx = _decode_fullsize(layer8b, CONFIGS["llama8b_decode"], sample=[0, 17, 63], phase=B.PS_PHASE_ANSWER)
+    assert min(ctx) >= 1024 and max(ctx) <= 4096
+
+
+def test_think_batch32_long_context_sampled_sequences(layer8b):
+    wl = CONFIGS["llama8b_think"]
+    ctx = [int(c) for c in gen.context_lengths(wl)]
+    longest = int(np.argmax(ctx))
+    _decode_fullsize(layer8b, wl, sample=sorted({0, longest}), phase=B.PS_PHASE_THINK)
+
+
+def test_think_mixed_step_sampled(layer8b):
+    _decode_fullsize(layer8b, CONFIGS["llama8b_think"], sample=[1, 31], phase=B.PS_PHASE_THINK, mixed=True)
