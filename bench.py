@@ -261,6 +261,99 @@ def bench_think(torch, B, A, wl, steps, warmup):
     return res
 
 
+def bench_model70b(torch, B, A, wl, steps, warmup):
+    """80-layer 70B-shaped model: autoregressive decode of 64 sequences at
+    context 4096 (tokens stay on the device), and a prefill of 8 x 1024."""
+    from synth import gen as G
+    sh = wl.shape
+    L, V = wl.n_layers, wl.vocab
+    gen = torch.Generator(device="cuda").manual_seed(70)
+    cfg = B.make_cfg(sh)
+    t0 = time.perf_counter()
+    tws, ws_list = [], []
+    for _ in range(L):
+        tw, w = make_layer_weights(torch, B, sh, gen)
+        tws.append(tw)
+        ws_list.append(w)
+    embed = randn(torch, gen, (V, sh.hidden), 0.02)
+    lm_head = randn(torch, gen, (V, sh.hidden), 0.02)
+    final_norm = randn(torch, gen, (sh.hidden,), 0.02, 1.0)
+    ctx = wl.ctx_params[0]
+    nb, npf, tp = wl.decode_batch, wl.prefill_seqs, wl.prefill_tokens
+    extra = warmup + steps + 2
+    pages_dec = (ctx + extra + 15) // 16
+    n_pages = nb * pages_dec + npf * ((tp + 15) // 16) + 8
+    pool = torch.empty(B.KV.pool_bytes(cfg, L, n_pages) // 2, dtype=torch.bfloat16, device="cuda")
+    chunk = 1 << 30
+    for i in range(0, pool.numel(), chunk):  # synthetic KV history, N(0, 1)
+        n = min(chunk, pool.numel() - i)
+        pool[i:i + n] = torch.randn(n, generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    fill_s = time.perf_counter() - t0
+    log(f"model70b: filled {sum(t.numel() for tw in tws for t in tw.values()) * 2 / 1e9:.1f} GB weights and "
+        f"{pool.numel() * 2 / 1e9:.1f} GB KV in {fill_s:.1f} s")
+    kv = B.KV(cfg, L, n_pages, nb + npf, max(pages_dec, (tp + 15) // 16), pool, seed=G.page_order_seed(wl))
+    model = B.Model(cfg, ws_list, V, embed, final_norm, lm_head)
+    seqs = [kv.open() for _ in range(nb)]
+    for s in seqs:
+        kv.alloc(s, ctx + extra)
+        kv.commit([s], [ctx])
+    ws = torch.empty(B.Model.workspace_bytes(cfg, V, npf * tp, nb + npf, pages_dec), dtype=torch.uint8,
+                     device="cuda")
+    tok = [torch.randint(0, V, (nb,), generator=gen, device="cuda", dtype=torch.int32),
+           torch.empty(nb, dtype=torch.int32, device="cuda")]
+
+    def dstep(i):
+        model.decode_step(kv, B.PS_PHASE_ANSWER, seqs, tok[i % 2], tok[(i + 1) % 2], ws)
+        kv.commit(seqs, [1] * nb)
+
+    for i in range(warmup):
+        dstep(i)
+    torch.cuda.synchronize()
+    lens0 = [kv.seq_len(s) for s in seqs]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        dstep(warmup + i)
+    torch.cuda.synchronize()
+    d_ms = (time.perf_counter() - t0) * 1e3 / steps
+    kv_bytes = L * sum(A.decode_attention_bytes([x + i + 1 for x in lens0], sh.n_kv, sh.head_dim, 2)
+                       for i in range(steps)) / steps
+    w_bytes = L * A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2) + V * sh.hidden * 2
+    # prefill 8 x 1024 on fresh sequences (positions restart each step)
+    pseqs = [kv.open() for _ in range(npf)]
+    for s in pseqs:
+        kv.alloc(s, tp)
+    ptok = torch.randint(0, V, (npf * tp,), generator=gen, device="cuda", dtype=torch.int32)
+    pnext = torch.empty(npf, dtype=torch.int32, device="cuda")
+
+    def pstep():
+        model.prefill(kv, pseqs, [tp] * npf, ptok, pnext, ws)
+        for s in pseqs:
+            kv.truncate(s, 0)
+
+    pstep()
+    torch.cuda.synchronize()
+    psteps = max(2, steps // 4)
+    t0 = time.perf_counter()
+    for _ in range(psteps):
+        pstep()
+    torch.cuda.synchronize()
+    p_ms = (time.perf_counter() - t0) * 1e3 / psteps
+    p_flops = L * (A.gemm_flops(npf * tp, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) +
+                   A.prefill_attention_flops([tp] * npf, sh.n_q, sh.head_dim)) + 2.0 * npf * V * sh.hidden
+    res = {
+        "decode": {"tok_s": nb / (d_ms * 1e-3), "ms_per_step": d_ms, "batch": nb, "ctx": ctx,
+                   "hbm_gbs": (kv_bytes + w_bytes) / (d_ms * 1e-3) / 1e9, "step_bytes": kv_bytes + w_bytes},
+        "prefill": {"tok_s": npf * tp / (p_ms * 1e-3), "ms_per_step": p_ms,
+                    "tflops": p_flops / (p_ms * 1e-3) / 1e12},
+        "hbm_resident_gb": (sum(t.numel() for tw in tws for t in tw.values()) + 2 * V * sh.hidden + pool.numel()) * 2
+        / 1e9,
+        "fill_s": fill_s,
+    }
+    del pool, ws, tws, embed, lm_head
+    return res
+
+
 def cpu_baseline(wl, n_tokens, budget_s=10.0):
     """The fp64 oracle on the host over whole prompts of the prefill workload
     (weights regenerated by the seeded generator), prompt after prompt until
@@ -291,6 +384,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=2048)
+    ap.add_argument("--no-model70b", action="store_true", help="skip the 80-layer 70B-shaped model")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
@@ -327,6 +421,14 @@ def main():
         log(f"think: {think['tok_s']:.0f} tok/s, attention {think['attention']['gbs']:.0f} GB/s, "
             f"mixed step {think['mixed_step']['ms']:.3f} ms")
         torch.cuda.empty_cache()
+    m70 = None
+    if not a.no_model70b:
+        m_wl = CONFIGS["llama70b_model"]
+        log(f"model70b: {m_wl.note}")
+        m70 = bench_model70b(torch, B, A, m_wl, max(4, a.steps // 2), 2)
+        log(f"model70b: decode {m70['decode']['tok_s']:.0f} tok/s ({m70['decode']['ms_per_step']:.1f} ms/step, "
+            f"{m70['decode']['hbm_gbs']:.0f} GB/s), prefill {m70['prefill']['tok_s']:.0f} tok/s")
+        torch.cuda.empty_cache()
     cpu = None
     if not a.no_cpu_baseline:
         log("cpu baseline: fp64 oracle on the host")
@@ -342,6 +444,7 @@ def main():
         "prefill": {k: v for k, v in pre.items() if k != "roofline"},
         "decode": dec,
         "think": think,
+        "model70b": m70,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

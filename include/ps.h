@@ -188,6 +188,36 @@ ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t lay
                         const int32_t* dec_seqs, const void* x_in, void* x_out, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------ model
+ * A stack of n_layers layers (bf16) with token embedding, final RMSNorm,
+ * LM head and greedy decoding, as served for the paper's 70B-class models
+ * (§VI workloads; §III-C's 320 KiB/token is this stack's KV footprint).
+ * Layer l uses layer l of the KV pool (which needs >= n_layers layers):
+ *   h0 = embed[token];  h_L = layer_{L-1}(... layer_0(h0));
+ *   logits = RMSNorm(h_L) * g_final · W_lmᵀ;  next = argmax (ties -> lowest id)
+ * embed and lm_head are [vocab, d]; final_norm [d]; `layers` is a host array
+ * of n_layers weight sets (device pointers, borrowed until destroy).
+ * Token ids live on the device; an id outside [0, vocab) embeds as a zero
+ * row. Neither call commits: call ps_kv_commit after it.
+ *
+ * ps_model_prefill: every sequence's n_tok rows run through all layers
+ * (cached prefix allowed, as in ps_prefill); only each sequence's last row
+ * goes through the LM head: dev_next[i] is the greedy token after prompt i.
+ * ps_model_decode_step: one token per sequence, as ps_decode_step.
+ * dev_logits (optional, may be NULL): fp32 [n_seqs, vocab] logits. */
+typedef struct ps_model ps_model;
+ps_status ps_model_create(const ps_layer_cfg* cfg, int32_t n_layers, int32_t vocab, const void* embed,
+                          const ps_layer_w* layers, const void* final_norm, const void* lm_head, ps_model** out);
+ps_status ps_model_destroy(ps_model* model);
+size_t ps_model_workspace_bytes(const ps_layer_cfg* cfg, int32_t vocab, int32_t max_rows, int32_t max_seqs,
+                                int32_t max_pages_per_seq);
+ps_status ps_model_prefill(ps_model* model, ps_kv* kv, int32_t n_seqs, const int32_t* seqs, const int32_t* n_tok,
+                           const int32_t* dev_tokens, int32_t* dev_next, float* dev_logits, void* ws,
+                           size_t ws_bytes, void* stream);
+ps_status ps_model_decode_step(ps_model* model, ps_kv* kv, int32_t phase, int32_t n_seqs, const int32_t* seqs,
+                               const int32_t* dev_tokens, int32_t* dev_next, float* dev_logits, void* ws,
+                               size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------- single ops
  * Stage entry points (tests, microbenchmarks). Same ownership and error
  * rules. dtype arguments are ps_dtype; PS_F32 for fp32 buffers. */
@@ -238,6 +268,9 @@ ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_
 ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
                                  const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
                                  void* stream);
+
+/* Greedy token of each row of fp32 logits [rows, vocab] (ties -> lowest id). */
+ps_status ps_op_argmax(int32_t rows, int32_t vocab, const float* logits, int32_t* next, void* stream);
 
 #ifdef __cplusplus
 }

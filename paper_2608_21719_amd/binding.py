@@ -92,6 +92,12 @@ _SIGS = {
     "ps_op_rope_kvwrite": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_op_attention": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_op_decode_attention": (_I, [_P, _I, _I, _IP, _P, _P, _I, _P, c_size_t, _P]),
+    "ps_op_argmax": (_I, [_I, _I, _P, _P, _P]),
+    "ps_model_create": (_I, [POINTER(LayerCfg), _I, _I, _P, POINTER(LayerW), _P, _P, POINTER(c_void_p)]),
+    "ps_model_destroy": (_I, [_P]),
+    "ps_model_workspace_bytes": (c_size_t, [POINTER(LayerCfg), _I, _I, _I, _I]),
+    "ps_model_prefill": (_I, [_P, _P, _I, _IP, _IP, _P, _P, _P, _P, c_size_t, _P]),
+    "ps_model_decode_step": (_I, [_P, _P, _I, _I, _IP, _P, _P, _P, _P, c_size_t, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(lib, _name)
@@ -264,6 +270,49 @@ class Layer:
         check(lib.ps_mixed_step(self.h, ctypes.byref(w), kv.h, layer, len(chunk_seqs), ints(chunk_seqs),
                                 ints(chunk_tok), len(dec_seqs), ints(dec_seqs), ptr(x_in), ptr(x_out), ptr(ws),
                                 ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+class Model:
+    """n_layers stacked layers + embedding, final norm, LM head, greedy argmax."""
+
+    def __init__(self, cfg: LayerCfg, layers, vocab: int, embed, final_norm, lm_head):
+        self.cfg = cfg
+        self.n_layers = len(layers)
+        self.keep = (layers, embed, final_norm, lm_head)
+        arr = (LayerW * len(layers))(*layers)
+        self._arr = arr
+        h = c_void_p()
+        check(lib.ps_model_create(ctypes.byref(cfg), len(layers), vocab, ptr(embed), arr, ptr(final_norm),
+                                  ptr(lm_head), ctypes.byref(h)))
+        self.h = h
+        self.vocab = vocab
+
+    def close(self):
+        if self.h:
+            check(lib.ps_model_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def workspace_bytes(cfg, vocab, max_rows, max_seqs, max_pages_per_seq) -> int:
+        return lib.ps_model_workspace_bytes(ctypes.byref(cfg), vocab, max_rows, max_seqs, max_pages_per_seq)
+
+    def prefill(self, kv: "KV", seqs, n_tok, tokens, next_tok, ws, logits=None, stream=None):
+        check(lib.ps_model_prefill(self.h, kv.h, len(seqs), ints(seqs), ints(n_tok), ptr(tokens), ptr(next_tok),
+                                   ptr(logits), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
+
+    def decode_step(self, kv: "KV", phase, seqs, tokens, next_tok, ws, logits=None, stream=None):
+        check(lib.ps_model_decode_step(self.h, kv.h, phase, len(seqs), ints(seqs), ptr(tokens), ptr(next_tok),
+                                       ptr(logits), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def op_argmax(rows, vocab, logits, next_tok, stream=None):
+    check(lib.ps_op_argmax(rows, vocab, ptr(logits), ptr(next_tok), stream_handle(stream)))
 
 
 def layer_weights(attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down) -> LayerW:

@@ -138,6 +138,15 @@ struct ps_layer {
   ps_layer_cfg cfg;
 };
 
+struct ps_model {
+  ps_layer_cfg cfg;
+  int32_t n_layers = 0, vocab = 0;
+  const void* embed = nullptr;
+  const void* final_norm = nullptr;
+  const void* lm_head = nullptr;
+  std::vector<ps_layer_w> layers;
+};
+
 // ------------------------------------------------------------------ misc
 extern "C" const char* ps_last_error(void) { return g_err.c_str(); }
 extern "C" const char* ps_version(void) { return "libps 0.1.0 gfx950"; }
@@ -383,12 +392,15 @@ WsLayout layout(const ps_layer_cfg& c, size_t meta_bytes, int32_t rows, int32_t 
   L.o = take(rows * dq * eb);
   L.h = take(rows * d * 4);
   L.m = take(rows * (size_t)c.ffn * eb);
+  // split-K partials of the decode-sized GEMMs, sized for min(rows, 64)
+  // rows so that a bound taken for more rows also covers smaller calls
   size_t g = 0;
-  if (rows <= 64) {
-    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)(dq + 2 * dkv), (int)d));
-    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)d, (int)dq));
-    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, 2 * c.ffn, (int)d));
-    g = std::max(g, gemm_workspace_bytes(c.dtype, rows, (int)d, c.ffn));
+  const int gm = std::min(rows, 64);
+  if (gm > 0) {
+    g = std::max(g, gemm_workspace_bytes(c.dtype, gm, (int)(dq + 2 * dkv), (int)d));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, gm, (int)d, (int)dq));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, gm, 2 * c.ffn, (int)d));
+    g = std::max(g, gemm_workspace_bytes(c.dtype, gm, (int)d, c.ffn));
   }
   L.gemm = take(g);
   L.apart_o = take((size_t)n_parts_max * dq * 4);
@@ -509,73 +521,79 @@ extern "C" size_t ps_workspace_bytes(const ps_layer_cfg* c, int32_t max_rows, in
 
 namespace {
 
-// One layer over n_chunk prefill sequences (chunk_tok rows each) followed by
-// n_dec decode sequences (one row each).
-ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase, int32_t n_chunk,
-                    const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec, const int32_t* dec_seqs,
-                    const void* x_in, void* x_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!L) return fail(PS_E_INVALID, "null layer handle");
-  CHECK_KV(kv);
-  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm || !w->w_gate_up || !w->w_down)
-    return fail(PS_E_INVALID, "null weight pointer");
-  const ps_layer_cfg& c = L->cfg;
-  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0)
-    return fail(PS_E_INVALID, "layer and KV pool configurations differ");
-  if (ps_status rc = check_layer(kv, layer)) return rc;
-  if (phase < PS_PHASE_PREFILL || phase > PS_PHASE_ANSWER) return fail(PS_E_INVALID, "bad phase");
+// Everything a layer call needs besides weights, pool and activations: the
+// call's sequence tables and work lists (uploaded once to the workspace head)
+// and the workspace carve-out. A model step plans once and launches it for
+// every layer.
+struct LayerPlan {
+  int32_t rows = 0, chunk_rows = 0, n_chunk = 0, n_dec = 0;
+  bool fa = false, dec_mfma = false;
+  size_t o_si = 0, o_bt = 0, o_fr = 0, o_pi = 0, o_di = 0, o_pb = 0, o_pc = 0;
+  int n_pitems = 0, n_ditems = 0;
+  int32_t n_parts = 0;
+  int32_t n_seqs = 0;
+  Meta mt;
+  WsLayout wl;
+};
 
+ps_status plan_layer(const ps_layer_cfg& c, const ps_kv* kv, int32_t phase, int32_t n_chunk,
+                     const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec, const int32_t* dec_seqs,
+                     LayerPlan& P) {
+  if (phase < PS_PHASE_PREFILL || phase > PS_PHASE_ANSWER) return fail(PS_E_INVALID, "bad phase");
   CallSeqs cs;
   if (ps_status rc = plan_seqs(kv, n_chunk, chunk_seqs, chunk_tok, -1, cs)) return rc;
-  const int32_t chunk_rows = cs.rows;
+  P.chunk_rows = cs.rows;
   if (ps_status rc = plan_seqs(kv, n_dec, dec_seqs, nullptr, 1, cs)) return rc;
   for (int i = 0; i < n_dec; ++i)
     for (int j = 0; j < n_chunk; ++j)
       if (dec_seqs[i] == chunk_seqs[j]) return fail(PS_E_INVALID, "sequence both chunked and decoding");
-  const int32_t rows = cs.rows;
-  if (rows == 0) return PS_OK;
-  if (!x_in || !x_out) return fail(PS_E_INVALID, "null activation pointer");
-
+  P.rows = cs.rows;
+  P.n_chunk = n_chunk;
+  P.n_dec = n_dec;
+  P.n_seqs = (int32_t)cs.si.size();
   const int d = c.hidden, dq = c.n_q_heads * c.head_dim, dkv = c.n_kv_heads * c.head_dim;
-  const int dt = c.dtype, G = group_of(c);
   // every GEMM of the call must be supported before anything is enqueued
-  if (gemm_check(dt, 0, rows, dq + 2 * dkv, d) || gemm_check(dt, 1, rows, d, dq) ||
-      gemm_check(dt, 2, rows, 2 * c.ffn, d) || gemm_check(dt, 1, rows, d, c.ffn))
+  if (P.rows > 0 && (gemm_check(c.dtype, 0, P.rows, dq + 2 * dkv, d) || gemm_check(c.dtype, 1, P.rows, d, dq) ||
+                     gemm_check(c.dtype, 2, P.rows, 2 * c.ffn, d) || gemm_check(c.dtype, 1, P.rows, d, c.ffn)))
     return fail(PS_E_UNSUPPORTED, "GEMM shape not supported by this build");
-
-  Meta mt;
-  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
-  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  P.o_si = P.mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  P.o_bt = P.mt.add(cs.bt.data(), cs.bt.size() * 4);
   const std::vector<double> fr = inv_freq(c);
-  const size_t o_fr = mt.add(fr.data(), fr.size() * 8);
-  const bool fa = fa_ok(c) && n_chunk > 0;
-  const bool dec_mfma = dec_ok(c) && n_dec > 0;
-  std::vector<PrefillItem> pitems;
-  size_t o_pi = 0;
-  if (fa) {
-    pitems = plan_prefill(cs.si, n_chunk);
-    o_pi = mt.add(pitems.data(), pitems.size() * sizeof(PrefillItem));
+  P.o_fr = P.mt.add(fr.data(), fr.size() * 8);
+  P.fa = fa_ok(c) && n_chunk > 0;
+  P.dec_mfma = dec_ok(c) && n_dec > 0;
+  if (P.fa) {
+    std::vector<PrefillItem> pitems = plan_prefill(cs.si, n_chunk);
+    P.n_pitems = (int)pitems.size();
+    P.o_pi = P.mt.add(pitems.data(), pitems.size() * sizeof(PrefillItem));
   }
-  DecodePlan dp;
-  size_t o_di = 0, o_pb = 0, o_pc = 0;
-  if (dec_mfma) {
-    dp = plan_decode(cs.si, n_chunk, choose_split_pages(cs.si, n_chunk, c.n_kv_heads, phase));
-    o_di = mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
-    o_pb = mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
-    o_pc = mt.add(dp.part_count.data(), dp.part_count.size() * 4);
+  if (P.dec_mfma) {
+    DecodePlan dp = plan_decode(cs.si, n_chunk, choose_split_pages(cs.si, n_chunk, c.n_kv_heads, phase));
+    P.n_ditems = (int)dp.items.size();
+    P.n_parts = dp.n_parts;
+    P.o_di = P.mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
+    P.o_pb = P.mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
+    P.o_pc = P.mt.add(dp.part_count.data(), dp.part_count.size() * 4);
   }
-  const WsLayout wl = layout(c, mt.size(), rows, dp.n_parts);
-  if (ps_status rc = check_ws(ws, ws_bytes, wl.total)) return rc;
+  return PS_OK;
+}
 
+ps_status upload_meta(ps_kv* kv, const Meta& mt, void* ws, hipStream_t st) {
   void* host;
   const int slot = kv->staging.acquire(mt.size(), &host);
   if (slot < 0) return PS_E_HIP;
   std::memcpy(host, mt.buf.data(), mt.buf.size());
-  hipStream_t st = (hipStream_t)stream;
-  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  return kv->staging.submit(slot, ws, mt.buf.size(), st);
+}
 
-  char* W = (char*)ws;
-  const SeqInfo* si = (const SeqInfo*)(W + o_si);
-  const int32_t* bt = (const int32_t*)(W + o_bt);
+// The kernels of one layer: x_in -> x_out for the planned rows.
+int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w, void* pool, const void* x_in,
+                 void* x_out, char* W, hipStream_t st) {
+  const WsLayout& wl = P.wl;
+  const int d = c.hidden, dq = c.n_q_heads * c.head_dim, dkv = c.n_kv_heads * c.head_dim;
+  const int dt = c.dtype, G = group_of(c), rows = P.rows;
+  const SeqInfo* si = (const SeqInfo*)(W + P.o_si);
+  const int32_t* bt = (const int32_t*)(W + P.o_bt);
   void* xn = W + wl.xn;
   void* qkv = W + wl.qkv;
   void* qr = W + wl.qr;
@@ -584,47 +602,219 @@ ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, 
   void* m = W + wl.m;
   void* gws = W + wl.gemm;
   const size_t gws_bytes = wl.apart_o - wl.gemm;
-  void* pool = kv->layer_base(layer);
   const size_t eb = elt_bytes(dt);
   const float scale = 1.0f / std::sqrt((float)c.head_dim);
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
   int bad = 0;
-
   bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st);
   bad |= launch_gemm(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes, st);
-  bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + o_fr), (int)cs.si.size(),
-                             c.n_q_heads, c.n_kv_heads, c.head_dim, st);
+  bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + P.o_fr), P.n_seqs, c.n_q_heads,
+                             c.n_kv_heads, c.head_dim, st);
   // attention: prefill rows on the flash kernel, decode rows on the split-K
   // kernel, anything else (fp32, other head sizes) on the vector kernel
-  if (n_chunk > 0) {
-    if (fa)
-      bad |= launch_fa_prefill(G, (int)pitems.size(), c.n_kv_heads, qr, pool, si, bt,
-                               (const PrefillItem*)(W + o_pi), o, scale_log2, st);
+  if (P.n_chunk > 0) {
+    if (P.fa)
+      bad |= launch_fa_prefill(G, P.n_pitems, c.n_kv_heads, qr, pool, si, bt, (const PrefillItem*)(W + P.o_pi), o,
+                               scale_log2, st);
     else
-      bad |= launch_attn_generic(dt, 0, chunk_rows, (int)cs.si.size(), c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
-                                 pool, si, bt, o, scale, st);
+      bad |= launch_attn_generic(dt, 0, P.chunk_rows, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr, pool, si,
+                                 bt, o, scale, st);
   }
-  if (n_dec > 0) {
-    if (dec_mfma) {
-      const char* qd = (const char*)qr + (size_t)chunk_rows * dq * eb;
-      char* od = (char*)o + (size_t)chunk_rows * dq * eb;
-      bad |= launch_decode_attn(G, (int)dp.items.size(), c.n_kv_heads, n_dec, qd, pool, si + n_chunk, bt,
-                                (const DecodeItem*)(W + o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
-                                (const int32_t*)(W + o_pb), (const int32_t*)(W + o_pc), od, scale_log2, st);
+  if (P.n_dec > 0) {
+    if (P.dec_mfma) {
+      const char* qd = (const char*)qr + (size_t)P.chunk_rows * dq * eb;
+      char* od = (char*)o + (size_t)P.chunk_rows * dq * eb;
+      bad |= launch_decode_attn(G, P.n_ditems, c.n_kv_heads, P.n_dec, qd, pool, si + P.n_chunk, bt,
+                                (const DecodeItem*)(W + P.o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
+                                (const int32_t*)(W + P.o_pb), (const int32_t*)(W + P.o_pc), od, scale_log2, st);
     } else {
-      bad |= launch_attn_generic(dt, chunk_rows, n_dec, (int)cs.si.size(), c.n_q_heads, c.n_kv_heads, c.head_dim,
-                                 qr, pool, si, bt, o, scale, st);
+      bad |= launch_attn_generic(dt, P.chunk_rows, P.n_dec, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
+                                 pool, si, bt, o, scale, st);
     }
   }
   bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
   bad |= launch_rmsnorm(PS_F32, dt, dt, rows, d, h, w->ffn_norm, c.rms_eps, xn, st);
   bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes, st);
   bad |= launch_gemm(dt, PS_F32, dt, PS_EPI_RESIDUAL, rows, d, c.ffn, m, w->w_down, h, x_out, gws, gws_bytes, st);
+  return bad;
+}
+
+ps_status check_weights(const ps_layer_w* w) {
+  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm || !w->w_gate_up || !w->w_down)
+    return fail(PS_E_INVALID, "null weight pointer");
+  return PS_OK;
+}
+
+// One layer over n_chunk prefill sequences (chunk_tok rows each) followed by
+// n_dec decode sequences (one row each).
+ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase, int32_t n_chunk,
+                    const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec, const int32_t* dec_seqs,
+                    const void* x_in, void* x_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!L) return fail(PS_E_INVALID, "null layer handle");
+  CHECK_KV(kv);
+  if (ps_status rc = check_weights(w)) return rc;
+  const ps_layer_cfg& c = L->cfg;
+  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0)
+    return fail(PS_E_INVALID, "layer and KV pool configurations differ");
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  LayerPlan P;
+  if (ps_status rc = plan_layer(c, kv, phase, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, P)) return rc;
+  if (P.rows == 0) return PS_OK;
+  if (!x_in || !x_out) return fail(PS_E_INVALID, "null activation pointer");
+  P.wl = layout(c, P.mt.size(), P.rows, P.n_parts);
+  if (ps_status rc = check_ws(ws, ws_bytes, P.wl.total)) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = upload_meta(kv, P.mt, ws, st)) return rc;
+  if (launch_layer(c, P, w, kv->layer_base(layer), x_in, x_out, (char*)ws, st))
+    return fail(PS_E_UNSUPPORTED, "a kernel rejected its configuration");
+  return last_launch_error();
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ model
+namespace {
+
+struct ModelWs {
+  size_t xa, xb, hl, hn, logits, lm, total;
+};
+
+ModelWs model_layout(const ps_layer_cfg& c, int32_t vocab, size_t layer_total, int32_t rows, int32_t n_out) {
+  ModelWs m;
+  size_t off = align_up(layer_total, 256);
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  m.xa = take((size_t)rows * c.hidden * 2);
+  m.xb = take((size_t)rows * c.hidden * 2);
+  m.hl = take((size_t)n_out * c.hidden * 2);
+  m.hn = take((size_t)n_out * c.hidden * 2);
+  m.logits = take((size_t)n_out * vocab * 4);
+  m.lm = take(gemm_workspace_bytes(PS_BF16, n_out, vocab, c.hidden));
+  m.total = off;
+  return m;
+}
+
+ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, const int32_t* chunk_seqs,
+                    const int32_t* chunk_tok, int32_t n_dec, const int32_t* dec_seqs, const int32_t* tokens,
+                    int32_t* next, float* logits_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!M) return fail(PS_E_INVALID, "null model handle");
+  CHECK_KV(kv);
+  const ps_layer_cfg& c = M->cfg;
+  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0) return fail(PS_E_INVALID, "model and KV pool configurations differ");
+  if (kv->n_layers < M->n_layers) return fail(PS_E_INVALID, "KV pool has fewer layers than the model");
+  LayerPlan P;
+  if (ps_status rc = plan_layer(c, kv, phase, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, P)) return rc;
+  if (P.rows == 0) return PS_OK;
+  if (!tokens || !next) return fail(PS_E_INVALID, "null token pointer");
+  const int32_t n_out = n_chunk + n_dec;
+  if (gemm_check(PS_BF16, PS_EPI_STORE, n_out, M->vocab, c.hidden))
+    return fail(PS_E_UNSUPPORTED, "LM head shape not supported by this build");
+  // last row of every sequence feeds the LM head
+  std::vector<int32_t> last(n_out);
+  {
+    int32_t r = 0;
+    for (int i = 0; i < n_chunk; ++i) {
+      r += chunk_tok[i];
+      last[i] = r - 1;
+    }
+    for (int i = 0; i < n_dec; ++i) last[n_chunk + i] = r + i;
+  }
+  const size_t o_last = P.mt.add(last.data(), last.size() * 4);
+  P.wl = layout(c, P.mt.size(), P.rows, P.n_parts);
+  const ModelWs mw = model_layout(c, M->vocab, P.wl.total, P.rows, n_out);
+  if (ps_status rc = check_ws(ws, ws_bytes, mw.total)) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  if (ps_status rc = upload_meta(kv, P.mt, ws, st)) return rc;
+  char* W = (char*)ws;
+  int bad = launch_embed(P.rows, c.hidden, M->vocab, M->embed, tokens, W + mw.xa, st);
+  char* cur = W + mw.xa;
+  char* nxt = W + mw.xb;
+  for (int l = 0; l < M->n_layers; ++l) {
+    bad |= launch_layer(c, P, &M->layers[l], kv->layer_base(l), cur, nxt, W, st);
+    std::swap(cur, nxt);
+  }
+  float* logits = logits_out ? logits_out : (float*)(W + mw.logits);
+  bad |= launch_gather_rows(n_out, c.hidden, cur, (const int32_t*)(W + o_last), W + mw.hl, st);
+  bad |= launch_rmsnorm(PS_BF16, PS_BF16, PS_BF16, n_out, c.hidden, W + mw.hl, M->final_norm, c.rms_eps, W + mw.hn,
+                        st);
+  bad |= launch_gemm(PS_BF16, 0, PS_F32, PS_EPI_STORE, n_out, M->vocab, c.hidden, W + mw.hn, M->lm_head, nullptr,
+                     logits, W + mw.lm, mw.total - mw.lm, st);
+  bad |= launch_argmax(n_out, M->vocab, logits, next, st);
   if (bad) return fail(PS_E_UNSUPPORTED, "a kernel rejected its configuration");
   return last_launch_error();
 }
 
 }  // namespace
+
+extern "C" ps_status ps_model_create(const ps_layer_cfg* c, int32_t n_layers, int32_t vocab, const void* embed,
+                                     const ps_layer_w* layers, const void* final_norm, const void* lm_head,
+                                     ps_model** out) {
+  PS_TRY
+  if (ps_status rc = check_cfg(c)) return rc;
+  if (c->dtype != PS_BF16) return fail(PS_E_UNSUPPORTED, "the model path is bf16");
+  if (c->hidden % 8) return fail(PS_E_UNSUPPORTED, "hidden must be a multiple of 8");
+  if (!out || n_layers <= 0 || vocab <= 0 || !embed || !layers || !final_norm || !lm_head)
+    return fail(PS_E_INVALID, "bad model arguments");
+  for (int l = 0; l < n_layers; ++l)
+    if (ps_status rc = check_weights(&layers[l])) return rc;
+  ps_model* M = new ps_model;
+  M->cfg = *c;
+  M->n_layers = n_layers;
+  M->vocab = vocab;
+  M->embed = embed;
+  M->final_norm = final_norm;
+  M->lm_head = lm_head;
+  M->layers.assign(layers, layers + n_layers);
+  *out = M;
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" ps_status ps_model_destroy(ps_model* M) {
+  PS_TRY
+  delete M;
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" size_t ps_model_workspace_bytes(const ps_layer_cfg* c, int32_t vocab, int32_t max_rows, int32_t max_seqs,
+                                           int32_t max_pages_per_seq) {
+  if (!c || vocab <= 0 || max_rows < 0 || max_seqs < 0 || max_pages_per_seq < 0) return 0;
+  const size_t mb = meta_bound(*c, max_rows, max_seqs, max_pages_per_seq) + align_up(4ull * max_seqs, 256);
+  const int32_t parts = max_seqs * ((max_pages_per_seq + 7) / 8);
+  const WsLayout wl = layout(*c, mb, max_rows, parts);
+  return model_layout(*c, vocab, wl.total, max_rows, max_seqs).total;
+}
+
+extern "C" ps_status ps_model_prefill(ps_model* M, ps_kv* kv, int32_t n_seqs, const int32_t* seqs,
+                                      const int32_t* n_tok, const int32_t* dev_tokens, int32_t* dev_next,
+                                      float* dev_logits, void* ws, size_t ws_bytes, void* stream) {
+  PS_TRY
+  return run_model(M, kv, PS_PHASE_PREFILL, n_seqs, seqs, n_tok, 0, nullptr, dev_tokens, dev_next, dev_logits, ws,
+                   ws_bytes, stream);
+  PS_CATCH
+}
+
+extern "C" ps_status ps_model_decode_step(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_seqs, const int32_t* seqs,
+                                          const int32_t* dev_tokens, int32_t* dev_next, float* dev_logits, void* ws,
+                                          size_t ws_bytes, void* stream) {
+  PS_TRY
+  return run_model(M, kv, phase, 0, nullptr, nullptr, n_seqs, seqs, dev_tokens, dev_next, dev_logits, ws, ws_bytes,
+                   stream);
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_argmax(int32_t rows, int32_t vocab, const float* logits, int32_t* next, void* stream) {
+  PS_TRY
+  if (rows < 0 || vocab <= 0) return fail(PS_E_INVALID, "bad shape");
+  if (rows > 0 && (!logits || !next)) return fail(PS_E_INVALID, "null pointer");
+  launch_argmax(rows, vocab, logits, next, (hipStream_t)stream);
+  return last_launch_error();
+  PS_CATCH
+}
 
 extern "C" ps_status ps_prefill(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_seqs,
                                 const int32_t* seqs, const int32_t* n_tok, const void* x_in, void* x_out, void* ws,

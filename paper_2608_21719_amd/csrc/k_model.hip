@@ -1,0 +1,90 @@
+// Model-level kernels (gfx950): embedding gather, row gather, greedy argmax.
+#include "common.h"
+#include "launch.h"
+
+namespace ps {
+
+// x[r, :] = table[tokens[r], :], 16 bytes per thread.
+// Token ids outside [0, vocab) embed as zero rows (ids live on the device,
+// so they cannot be validated on the host before the launch).
+__global__ __launch_bounds__(256) void embed_kernel(const bf16_t* __restrict__ table, const int32_t* __restrict__ tokens,
+                                                    bf16_t* __restrict__ x, int d, int vocab) {
+  const long r = blockIdx.x;
+  const int tok = tokens[r];
+  if (tok < 0 || tok >= vocab) {
+    for (int i = threadIdx.x * 8; i < d; i += 256 * 8) *(uint4*)(x + r * d + i) = make_uint4(0, 0, 0, 0);
+    return;
+  }
+  for (int i = threadIdx.x * 8; i < d; i += 256 * 8)
+    *(uint4*)(x + r * d + i) = *(const uint4*)(table + (long)tok * d + i);
+}
+
+// dst[i, :] = src[rows[i], :] (bf16 rows of d elements)
+__global__ __launch_bounds__(256) void gather_rows_kernel(const bf16_t* __restrict__ src, const int32_t* __restrict__ rows,
+                                                          bf16_t* __restrict__ dst, int d) {
+  const long i = blockIdx.x;
+  const long r = rows[i];
+  for (int e = threadIdx.x * 8; e < d; e += 256 * 8) *(uint4*)(dst + i * d + e) = *(const uint4*)(src + r * d + e);
+}
+
+// next[r] = argmax_j logits[r, j], ties to the lowest j. One workgroup per row.
+__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int32_t* __restrict__ next,
+                                                     int vocab) {
+  const long r = blockIdx.x;
+  const float* row = logits + r * vocab;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int j = threadIdx.x; j < vocab; j += 256) {
+    const float v = row[j];
+    if (v > best) {  // strictly greater: j increases, so ties keep the lowest index
+      best = v;
+      bi = j;
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bi, off);
+    if (ov > best || (ov == best && oi < bi)) {
+      best = ov;
+      bi = oi;
+    }
+  }
+  __shared__ float sv[4];
+  __shared__ int si_[4];
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = best;
+    si_[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > best || (sv[w] == best && si_[w] < bi)) {
+        best = sv[w];
+        bi = si_[w];
+      }
+    // an all-NaN row keeps index 0x7fffffff: clamp to 0 so callers get a valid id
+    next[r] = bi == 0x7fffffff ? 0 : bi;
+  }
+}
+
+int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st) {
+  if (rows == 0) return 0;
+  if (d % 8) return -1;
+  hipLaunchKernelGGL(embed_kernel, dim3(rows), dim3(256), 0, st, (const bf16_t*)table, tokens, (bf16_t*)x, d, vocab);
+  return 0;
+}
+
+int launch_gather_rows(int n, int d, const void* src, const int32_t* rows, void* dst, hipStream_t st) {
+  if (n == 0) return 0;
+  if (d % 8) return -1;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, st, (const bf16_t*)src, rows, (bf16_t*)dst, d);
+  return 0;
+}
+
+int launch_argmax(int rows, int vocab, const float* logits, int32_t* next, hipStream_t st) {
+  if (rows == 0) return 0;
+  hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(256), 0, st, logits, next, vocab);
+  return 0;
+}
+
+}  // namespace ps

@@ -9,7 +9,12 @@ from synth import gen
 
 BF16_TOL_ABS, BF16_TOL_REL = 2e-2, 1e-2      # stage-level bound for bf16 outputs
 F32_TOL_ABS, F32_TOL_REL = 1e-4, 1e-4        # fp32 layer bound
-NORMWISE_TOL = 1e-2                           # end-to-end bf16 layer bound
+NORMWISE_TOL = 1e-2                           # end-to-end bf16 layer bound (d <= 4096)
+# d = 8192, F = 28672: an fp32 emulation with bf16 rounding at exactly the
+# device's rounding points (GEMM inputs, q/k/v, P, o, m, layer output) reaches
+# normwise max 1.15e-2 / rms 1.01e-2 against fp64 on the 256-token prompt of
+# the 70B-shaped layer; the end-to-end bound there is 2e-2
+NORMWISE_TOL_70B = 2e-2
 
 
 def torch_mod():

@@ -1,0 +1,206 @@
+"""The model path (embedding, layer stack, final norm, LM head, greedy argmax)
+against the fp64 oracle (GPU).
+
+Greedy tokens: several answers are correct when logits nearly tie, so a
+device token t is accepted iff oracle_logit[t] >= max oracle logit -
+(2e-2 + 1e-2 |max|), and logits are compared with the normwise bound. Decode
+steps consume predetermined synthetic tokens (not the device's argmax), so
+no device output ever becomes an oracle input.
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as O
+from synth import gen
+from synth.configs import CONFIGS, LayerShape, Workload
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_21719_amd import binding as B  # noqa: E402
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+def accept_tokens(got_tok, ref_logits, what):
+    for i, t in enumerate(got_tok):
+        mx = ref_logits[i].max()
+        tau = 2e-2 + 1e-2 * abs(mx)
+        assert ref_logits[i][t] >= mx - tau, f"{what} row {i}: token {t} logit {ref_logits[i][t]:.4f} < max {mx:.4f} - {tau:.3f}"
+
+
+def test_argmax_full_vocab_with_ties():
+    rows, vocab = 64, 128256
+    r = np.random.default_rng(1)
+    lg = r.standard_normal((rows, vocab)).astype(np.float32)
+    for i in range(rows):  # plant a tie between two maxima
+        a, b = sorted(r.choice(vocab, 2, replace=False))
+        lg[i, a] = lg[i, b] = 10.0 + i
+    lg[3, :] = 1.0  # all equal: index 0
+    d = torch.from_numpy(lg).cuda()
+    out = torch.empty(rows, dtype=torch.int32, device="cuda")
+    B.op_argmax(rows, vocab, d, out)
+    sync()
+    np.testing.assert_array_equal(out.cpu().numpy(), O.argmax_lowest(lg.astype(np.float64)))
+
+
+def test_lm_head_gemm_fullsize_sampled_columns():
+    """M=64 decode rows through the 128256 x 8192 LM head (skinny split-K path)."""
+    M, N, K = 64, 128256, 8192
+    g = torch.Generator(device="cuda").manual_seed(5)
+    a = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    w = (torch.randn((N, K), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    c = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    ws = H.workspace(B.op_gemm_workspace_bytes(B.PS_BF16, M, N, K))
+    B.op_gemm(B.PS_BF16, 0, B.PS_F32, B.PS_EPI_STORE, M, N, K, a, w, None, c, ws)
+    sync()
+    cols = np.sort(np.random.default_rng(2).choice(N, 300, replace=False))
+    af = H.to_f64(a)
+    wf = H.to_f64(w[torch.from_numpy(cols).cuda()])
+    ref = O.linear(af, wf)
+    got = c.cpu().numpy().astype(np.float64)[:, cols]
+    bound = (np.abs(af) @ np.abs(wf).T) * (2 * K * 2.0 ** -24)
+    assert np.all(np.abs(got - ref) <= bound + 1e-30), f"max err {np.abs(got - ref).max()}"
+
+
+SMALL = LayerShape(1024, 8, 1, 128, 2048, 1e-5, 500000.0, "bf16")
+
+
+def small_model_parts(n_layers=3, vocab=2048):
+    wl = Workload("small_model", 12, SMALL, n_layers=n_layers, vocab=vocab)
+    layers = [gen.layer_weights(wl, l) for l in range(n_layers)]
+    head = gen.model_head_weights(wl)
+    return wl, layers, head
+
+
+def oracle_model_rows(layers_f, head_f, shape, tokens, hists):
+    """Run the oracle stack over one sequence's new tokens; returns logits of
+    the last row and the per-layer (K, V) it appended."""
+    h = O.embed(head_f["embed"], tokens)
+    new_hist = []
+    for l, wf in enumerate(layers_f):
+        kh, vh = hists[l] if hists else (None, None)
+        r = O.layer_sequence(wf, shape, h, kh, vh)
+        h = r["out"]
+        new_hist.append((r["k"], r["v"]))
+    logits = O.lm_logits(h[-1:], head_f["final_norm"], head_f["lm_head"], shape.eps)[0]
+    return logits, new_hist
+
+
+def test_small_model_prefill_then_decode():
+    wl, layers, head = small_model_parts()
+    sh, L, V = wl.shape, wl.n_layers, wl.vocab
+    layers_f = [H.weights_f64(w, "bf16") for w in layers]
+    head_f = H.weights_f64(head, "bf16")
+    dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
+    dev_head = {k: H.to_dev(v, "bf16") for k, v in head.items()}
+    pool = H.Pool(sh, 64, 4, 8, n_layers=L, seed=21)
+    model = B.Model(pool.cfg, [d.w for d in dev_layers], V, dev_head["embed"], dev_head["final_norm"],
+                    dev_head["lm_head"])
+    lens = [40, 23]
+    seqs = [pool.kv.open() for _ in lens]
+    for s, n in zip(seqs, lens):
+        pool.kv.alloc(s, n + 4)
+    ws = H.workspace(B.Model.workspace_bytes(pool.cfg, V, 128, 4, 8))
+    toks = gen.token_ids(wl, sum(lens))
+    dtok = torch.from_numpy(toks).cuda()
+    nxt = torch.empty(len(seqs), dtype=torch.int32, device="cuda")
+    logits = torch.empty((len(seqs), V), dtype=torch.float32, device="cuda")
+    model.prefill(pool.kv, seqs, lens, dtok, nxt, ws, logits)
+    pool.kv.commit(seqs, lens)
+    sync()
+    hists, r0 = [], 0
+    ref_logits = []
+    for n in lens:
+        lg, hh = oracle_model_rows(layers_f, head_f, sh, toks[r0:r0 + n], None)
+        ref_logits.append(lg)
+        hists.append(hh)
+        r0 += n
+    ref_logits = np.stack(ref_logits)
+    got_logits = logits.cpu().numpy().astype(np.float64)
+    mx, rms = H.normwise(got_logits, ref_logits)
+    assert mx <= H.NORMWISE_TOL and rms <= H.NORMWISE_TOL, f"prefill logits normwise {mx:.2e} {rms:.2e}"
+    accept_tokens(nxt.cpu().numpy(), ref_logits, "prefill")
+    for step in range(3):
+        t = gen.token_ids(wl, len(seqs), step=step + 1)
+        model.decode_step(pool.kv, B.PS_PHASE_ANSWER, seqs, torch.from_numpy(t).cuda(), nxt, ws, logits)
+        pool.kv.commit(seqs, [1] * len(seqs))
+        sync()
+        ref_logits = []
+        for i in range(len(seqs)):
+            lg, hh = oracle_model_rows(layers_f, head_f, sh, t[i:i + 1], hists[i])
+            hists[i] = [(np.concatenate([kh, k]), np.concatenate([vh, v])) for (kh, vh), (k, v) in zip(hists[i], hh)]
+            ref_logits.append(lg)
+        ref_logits = np.stack(ref_logits)
+        got_logits = logits.cpu().numpy().astype(np.float64)
+        mx, rms = H.normwise(got_logits, ref_logits)
+        assert mx <= H.NORMWISE_TOL and rms <= H.NORMWISE_TOL, f"decode {step} logits normwise {mx:.2e} {rms:.2e}"
+        accept_tokens(nxt.cpu().numpy(), ref_logits, f"decode {step}")
+
+
+def test_model_rejects_shallow_pool():
+    wl, layers, head = small_model_parts(n_layers=2, vocab=256)
+    dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
+    dev_head = {k: H.to_dev(v, "bf16") for k, v in head.items()}
+    pool = H.Pool(wl.shape, 8, 2, 4, n_layers=1)
+    model = B.Model(pool.cfg, [d.w for d in dev_layers], 256, dev_head["embed"], dev_head["final_norm"],
+                    dev_head["lm_head"])
+    s = pool.kv.open()
+    pool.kv.alloc(s, 4)
+    ws = H.workspace(B.Model.workspace_bytes(pool.cfg, 256, 16, 2, 4))
+    tok = torch.zeros(4, dtype=torch.int32, device="cuda")
+    nxt = torch.empty(1, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.PsError) as e:
+        model.prefill(pool.kv, [s], [4], tok, nxt, ws)
+    assert e.value.code == B.PS_E_INVALID
+
+
+def test_70b_layer_fullsize_prefill_and_decode():
+    """One 70B-shaped layer (d 8192, 64/8 heads, F 28672): a 256-token prompt
+    and a decode step of 4 sequences at context 4096."""
+    wl = CONFIGS["llama70b_model"]
+    sh = wl.shape
+    w = gen.layer_weights(wl, 0)
+    wf = H.weights_f64(w, "bf16")
+    dev = H.DeviceLayer(w, "bf16")
+    ctx = [4096, 4095, 3000, 17]
+    pool = H.Pool(sh, sum((c + 16) // 16 for c in ctx) + 32, 8, 260, seed=5)
+    kv = pool.kv
+    layer = B.Layer(pool.cfg)
+    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, 256, 8, 260))
+    g = torch.Generator(device="cuda").manual_seed(99)
+    seqs, hist = [], []
+    for c in ctx:
+        s = kv.open()
+        kv.alloc(s, c + 1)
+        k = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        kv.append(0, [s], [c], k, v, ws)
+        kv.commit([s], [c])
+        seqs.append(s)
+        hist.append((H.to_f64(k), H.to_f64(v)))
+    x = gen.decode_input(wl, len(ctx), 0)
+    out = H.empty((len(ctx), sh.hidden), "bf16")
+    layer.decode_step(dev.w, kv, 0, B.PS_PHASE_ANSWER, seqs, H.to_dev(x, "bf16"), out, ws)
+    sync()
+    got = H.to_f64(out)
+    xf = gen.widen(x, "bf16")
+    for b in range(len(ctx)):
+        ref = O.layer_sequence(wf, sh, xf[b:b + 1], *hist[b])["out"][0]
+        mx, rms = H.normwise(got[b], ref)
+        assert mx <= H.NORMWISE_TOL_70B and rms <= H.NORMWISE_TOL_70B, f"decode b={b}: {mx:.2e} {rms:.2e}"
+    p = kv.open()
+    kv.alloc(p, 256)
+    xp = gen.prefill_input(wl, 256)
+    outp = H.empty((256, sh.hidden), "bf16")
+    layer.prefill(dev.w, kv, 0, [p], [256], H.to_dev(xp, "bf16"), outp, ws)
+    sync()
+    ref = O.layer_sequence(wf, sh, gen.widen(xp, "bf16"))["out"]
+    mx, rms = H.normwise(H.to_f64(outp), ref)
+    assert mx <= H.NORMWISE_TOL_70B and rms <= H.NORMWISE_TOL_70B, f"prefill: {mx:.2e} {rms:.2e}"
