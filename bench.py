@@ -121,7 +121,9 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
         "tok_s": tokens / (ms * 1e-3), "ms_per_step": ms,
         "layer_tflops": (total_gemm + attn) / (ms * 1e-3) / 1e12,
         "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K},
-        "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s", None).as_dict(),
+        "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s",
+                               measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
+                               ).as_dict(),
     }
     del pool, ws, tw, x, out, hn, m
     return res
@@ -183,7 +185,9 @@ def bench_decode(torch, B, A, wl, steps, warmup):
         "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
         "step_bytes": kv_bytes + w_bytes,
         "attention": {"us": a_ms * 1e3, "gbs": a_gbs, "bytes": a_bytes},
-        "roofline": A.Roofline("hbm", a_gbs, A.HBM_PEAK_GBS, "GB/s", None).as_dict(),
+        "roofline": A.Roofline("hbm", a_gbs, A.HBM_PEAK_GBS, "GB/s",
+                               measured_traffic("decode_attention_b64", "paper_2608_21719_amd/csrc/k_attn_decode.hip")
+                               ).as_dict(),
     }
     del pool, ws, tw, x, out, aws
     return res
@@ -376,6 +380,23 @@ def cpu_baseline(wl, n_tokens, budget_s=10.0):
                       f"fp64 numpy, {dt:.1f} s"}
 
 
+def measured_traffic(kernel_key, source_file):
+    """HBM bytes per launch of a kernel from profiles/traffic.json (two rocprof
+    --pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a known-size copy), or
+    None when the kernel's source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(kernel_key)
+    if not rec:
+        return None
+    src = os.path.join(ROOT, source_file)
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -385,6 +406,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--no-model70b", action="store_true", help="skip the 80-layer 70B-shaped model")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one 1 GiB device copy first (known bytes, to scale rocprof counters)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
@@ -401,6 +424,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if a.calib_copy:
+        # int32 -> fp32 conversion copy: reads exactly 1 GiB, writes exactly 1 GiB
+        src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     pre_wl = CONFIGS["llama8b_prefill"]
     dec_wl = CONFIGS["llama8b_decode"]
     log(f"prefill: {pre_wl.note}")
