@@ -66,12 +66,19 @@ __device__ __forceinline__ void load_lds16(const bf16_t* g, bf16_t* lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-// s_waitcnt with only vmcnt = n (n < 64), other counters not waited on
+// s_waitcnt vmcnt(n) lgkmcnt(0): this wave's global->LDS fills older than
+// its n most recent have landed, and its own LDS reads have returned.
 template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
 }
+
+// Workgroup barrier without the release/acquire fences of __syncthreads():
+// those wait for every outstanding global->LDS fill (vmcnt(0)) and would
+// collapse a ring deeper than two stages. Callers wait explicitly first; the
+// memory clobber keeps LDS accesses on their side of the barrier.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <class CF, int EPI, typename TR, typename TC>
 __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
@@ -128,42 +135,80 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
       load_lds16(gb[i] + k0, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
   };
 
-  f32x16_t acc[CF::FM][CF::FN];
+  // operand fragments, double-buffered in registers across 16-wide k steps
+  constexpr int FM = CF::FM, FN = CF::FN, KK = BK / 16;
+  static_assert(KK % 2 == 0, "register double-buffering alternates buffers by k-step parity");
+  bf16x8_t fa[2][FM], fb[2][FN];
+  auto frags = [&](int slot, int kk, int p) {
+    const bf16_t* a = smem + slot * CF::STAGE_ELTS;
+    const bf16_t* b = a + CF::A_ELTS;
 #pragma unroll
-  for (int i = 0; i < CF::FM; ++i)
+    for (int i = 0; i < FM; ++i)
+      fa[p][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 32 + c, 2 * kk + g)));
 #pragma unroll
-    for (int j = 0; j < CF::FN; ++j)
+    for (int j = 0; j < FN; ++j)
+      fb[p][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 32 + c, 2 * kk + g)));
+  };
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  auto mfmas = [&](int p) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+  };
+  // issue order for one k step: the next step's LDS reads spread evenly
+  // between this step's MFMAs, so read latency hides under matrix work
+  auto interleave = [&]() {
+    constexpr int RATIO = (FM * FN) / (FM + FN) > 0 ? (FM * FN) / (FM + FN) : 1;
+#pragma unroll
+    for (int q = 0; q < FM + FN; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, RATIO, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // LDS read
+    }
+    if constexpr (FM * FN > RATIO * (FM + FN))
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - RATIO * (FM + FN), 0);
+  };
 
   const int KT = K / BK;
-  // prologue: stages 0 .. STAGES-2 in flight
+  // prologue: stages 0 .. STAGES-2 in flight; stage 0 landed everywhere;
+  // stage STAGES-1 issued; fragments of (stage 0, k step 0) requested
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < KT) gload(st * BK, st);
+  if (STAGES - 2 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
+  else wait_vmcnt_lgkm0<0>();
+  lds_barrier();
+  if (STAGES - 1 < KT) gload((STAGES - 1) * BK, STAGES - 1);
+  frags(0, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
-    // stage kt has landed once at most (STAGES-2) later stages are pending
-    if (kt + STAGES - 2 < KT) wait_vmcnt<(STAGES - 2) * CF::LOADS>();
-    else wait_vmcnt<0>();
-    __syncthreads();
-    // refill the slot consumed in iteration kt-1
-    if (kt + STAGES - 1 < KT) gload((kt + STAGES - 1) * BK, (kt + STAGES - 1) % STAGES);
-    const bf16_t* a = smem + (kt % STAGES) * CF::STAGE_ELTS;
-    const bf16_t* b = a + CF::A_ELTS;
+    const int slot = kt % STAGES;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8_t af[CF::FM], bfr[CF::FN];
-#pragma unroll
-      for (int i = 0; i < CF::FM; ++i)
-        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 32 + c, 2 * kk + g)));
-#pragma unroll
-      for (int j = 0; j < CF::FN; ++j)
-        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 32 + c, 2 * kk + g)));
-#pragma unroll
-      for (int i = 0; i < CF::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < CF::FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    for (int kk = 0; kk < KK; ++kk) {
+      const int p = kk & 1;
+      if (kk < KK - 1) {
+        frags(slot, kk + 1, p ^ 1);
+        mfmas(p);
+        interleave();
+      } else {
+        mfmas(p);
+        if (kt + 1 < KT) {
+          // stage kt+1 has landed for this wave and this wave's reads of
+          // stage kt have returned; after the barrier both hold for all
+          // waves, so slot kt may be refilled with stage kt+STAGES
+          if (kt + STAGES - 1 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
+          else wait_vmcnt_lgkm0<0>();
+          lds_barrier();
+          if (kt + STAGES < KT) gload((kt + STAGES) * BK, slot);
+          frags((kt + 1) % STAGES, 0, p ^ 1);
+        }
+      }
     }
   }
 
