@@ -170,12 +170,14 @@ def bench_decode(torch, B, A, wl, steps, warmup):
                    for i in range(steps)) / steps
     w_bytes = A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2)
 
-    # dominant kernel: split-K decode attention (+ its combine), same stream
+    # dominant kernel: split-K decode attention + its split combine, timed
+    # alone (work list planned once, as for the layers of one step)
     q = randn(torch, gen, (nb, sh.n_q, sh.head_dim))
     o = torch.empty((nb, sh.d_q), dtype=torch.bfloat16, device="cuda")
     aws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
     timer = EventTimer(torch)
-    a_ms = timer(lambda: B.op_decode_attention(kv, 0, seqs, q, o, aws), iters=max(10, steps))
+    B.op_decode_plan(kv, seqs, aws)
+    a_ms = timer(lambda: B.op_decode_run(kv, 0, q, o, aws), iters=max(20, steps))
     lens = [kv.seq_len(s) for s in seqs]
     a_bytes = A.decode_attention_bytes([L + 1 for L in lens], sh.n_kv, sh.head_dim, 2)
     a_gbs = a_bytes / (a_ms * 1e-3) / 1e9
@@ -237,7 +239,8 @@ def bench_think(torch, B, A, wl, steps, warmup):
     q = randn(torch, gen, (nb, sh.n_q, sh.head_dim))
     o = torch.empty((nb, sh.d_q), dtype=torch.bfloat16, device="cuda")
     timer = EventTimer(torch)
-    a_ms = timer(lambda: B.op_decode_attention(kv, 0, seqs, q, o, ws), iters=max(10, steps))
+    B.op_decode_plan(kv, seqs, ws)
+    a_ms = timer(lambda: B.op_decode_run(kv, 0, q, o, ws), iters=max(20, steps))
     a_bytes = A.decode_attention_bytes([kv.seq_len(s) + 1 for s in seqs], sh.n_kv, sh.head_dim, 2)
 
     # mixed step: chunk rows first, then one row per decoding sequence

@@ -264,10 +264,28 @@ ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_
 /* Split-K decode attention: one query row per sequence at position len
  * (the row's own K/V already written there, not yet committed), attending
  * over keys 0..len. q [n_seqs, n_q, hd], o [n_seqs, n_q * hd].
- * split_pages = pages per split (0 = library choice). */
+ * split_pages = pages per split (0 = library choice). PS_E_UNSUPPORTED when
+ * the splits come to more than 65535 work items (one grid row each). */
 ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
                                  const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
                                  void* stream);
+
+/* The same attention as plan + run, for a step whose KV pool does not change
+ * between layers (plan once, run per layer; also how a caller times the
+ * attention kernels alone).
+ * ps_op_decode_plan: checks the sequences, picks the splits and uploads the
+ * work list (sequence records, page ids, splits) into ws on `stream`; the
+ * plan is recorded on the handle, replacing any earlier one (a failed call
+ * leaves none). Workspace need and errors as ps_op_decode_attention.
+ * ps_op_decode_run: launches the attention of one layer from the plan
+ * (q [n_seqs, n_q, hd] in the planned sequence order, o [n_seqs, n_q * hd]).
+ * PS_E_INVALID without a plan, with a workspace other than the planned one,
+ * or after any commit, truncate or free on the handle since the plan. The
+ * planned work list must stay untouched in ws while runs use it. */
+ps_status ps_op_decode_plan(ps_kv* kv, int32_t n_seqs, const int32_t* seqs, int32_t split_pages, void* ws,
+                            size_t ws_bytes, void* stream);
+ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
+                           void* stream);
 
 /* Greedy token of each row of fp32 logits [rows, vocab] (ties -> lowest id). */
 ps_status ps_op_argmax(int32_t rows, int32_t vocab, const float* logits, int32_t* next, void* stream);

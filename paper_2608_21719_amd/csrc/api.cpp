@@ -119,6 +119,16 @@ struct Meta {
 };
 }  // namespace
 
+// Host record of the last ps_op_decode_plan on a handle: where its work
+// list sits in the caller's workspace and the pool state it was made for.
+struct DecodeAttnPlan {
+  const void* ws = nullptr;
+  size_t ws_need = 0;
+  uint64_t gen = 0;
+  int32_t n_seqs = 0, n_items = 0;
+  size_t o_si = 0, o_bt = 0, o_di = 0, o_pb = 0, o_pc = 0, off_po = 0, off_pml = 0;
+};
+
 struct ps_kv {
   ps_layer_cfg cfg;
   int32_t n_layers;
@@ -126,6 +136,7 @@ struct ps_kv {
   size_t layer_elts;  // elements per layer
   KvPool meta;
   Staging staging;
+  DecodeAttnPlan dplan;
   ps_kv(const ps_layer_cfg& c, int32_t nl, int32_t np, int32_t ms, int32_t mp, void* p, uint64_t seed)
       : cfg(c), n_layers(nl), pool(p),
         layer_elts((size_t)np * c.n_kv_heads * 2 * PS_PAGE_TOKENS * c.head_dim), meta(np, ms, mp, seed) {}
@@ -314,11 +325,20 @@ int32_t choose_split_pages(const std::vector<SeqInfo>& si, size_t first, int n_k
   (void)phase;
   long total = 0;
   for (size_t b = first; b < si.size(); ++b) total += (si[b].kv_before + si[b].n_new + 15) / 16;
-  // about 2048 workgroups over the chip, at least 8 pages per split
-  const long target_items = std::max(1, 2048 / std::max(1, n_kv));
+  // about 3072 workgroups over the chip (a dozen per CU), at least 8 pages per split
+  const long target_items = std::max(1, 3072 / std::max(1, n_kv));
   long sp = (total + target_items - 1) / target_items;
   sp = std::max<long>(sp, 8);
   sp = (sp + 3) / 4 * 4;
+  // the work-item index is a grid y coordinate (at most 65535): widen the
+  // splits until the items fit (a batch of more sequences than that is
+  // rejected by the launcher)
+  auto n_items = [&](long spl) {
+    long n = 0;
+    for (size_t b = first; b < si.size(); ++b) n += ((si[b].kv_before + si[b].n_new + 15) / 16 + spl - 1) / spl;
+    return n;
+  };
+  while (n_items(sp) > kMaxDecodeItems && sp < (1L << 24)) sp *= 2;
   return (int32_t)sp;
 }
 
@@ -569,6 +589,8 @@ ps_status plan_layer(const ps_layer_cfg& c, const ps_kv* kv, int32_t phase, int3
   }
   if (P.dec_mfma) {
     DecodePlan dp = plan_decode(cs.si, n_chunk, choose_split_pages(cs.si, n_chunk, c.n_kv_heads, phase));
+    if ((long)dp.items.size() > kMaxDecodeItems)
+      return fail(PS_E_UNSUPPORTED, "decode batch exceeds 65535 attention work items");
     P.n_ditems = (int)dp.items.size();
     P.n_parts = dp.n_parts;
     P.o_di = P.mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
@@ -951,44 +973,79 @@ extern "C" ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, c
   PS_CATCH
 }
 
-extern "C" ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
-                                            const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
-                                            void* stream) {
+extern "C" ps_status ps_op_decode_plan(ps_kv* kv, int32_t n_seqs, const int32_t* seqs, int32_t split_pages,
+                                       void* ws, size_t ws_bytes, void* stream) {
   PS_TRY CHECK_KV(kv);
-  if (ps_status rc = check_layer(kv, layer)) return rc;
+  kv->dplan = DecodeAttnPlan{};
   const ps_layer_cfg& c = kv->cfg;
   if (!dec_ok(c)) return fail(PS_E_UNSUPPORTED, "split-K decode attention needs bf16, head_dim 128, G <= 16");
   if (split_pages < 0) return fail(PS_E_INVALID, "negative split_pages");
   CallSeqs cs;
   if (ps_status rc = plan_seqs(kv, n_seqs, seqs, nullptr, 1, cs)) return rc;
-  if (n_seqs > 0 && (!q || !o)) return fail(PS_E_INVALID, "null pointer");
   Meta mt;
-  const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
-  const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
+  DecodeAttnPlan pl;
+  pl.o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
+  pl.o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
   const int32_t sp = split_pages > 0 ? split_pages : choose_split_pages(cs.si, 0, c.n_kv_heads, PS_PHASE_ANSWER);
   DecodePlan dp = plan_decode(cs.si, 0, sp);
-  const size_t o_di = mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
-  const size_t o_pb = mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
-  const size_t o_pc = mt.add(dp.part_count.data(), dp.part_count.size() * 4);
+  if ((long)dp.items.size() > kMaxDecodeItems)
+    return fail(PS_E_UNSUPPORTED, "more than 65535 attention work items: use larger split_pages");
+  pl.o_di = mt.add(dp.items.data(), dp.items.size() * sizeof(DecodeItem));
+  pl.o_pb = mt.add(dp.part_begin.data(), dp.part_begin.size() * 4);
+  pl.o_pc = mt.add(dp.part_count.data(), dp.part_count.size() * 4);
   const size_t dq = (size_t)c.n_q_heads * c.head_dim;
-  const size_t off_po = mt.size();
-  const size_t off_pml = align_up(off_po + (size_t)dp.n_parts * dq * 4, 256);
-  const size_t need = align_up(off_pml + (size_t)dp.n_parts * c.n_q_heads * 2 * 4, 256);
-  if (ps_status rc = check_ws(ws, ws_bytes, need)) return rc;
-  if (n_seqs == 0) return PS_OK;
-  void* host;
-  const int slot = kv->staging.acquire(mt.size(), &host);
-  if (slot < 0) return PS_E_HIP;
-  std::memcpy(host, mt.buf.data(), mt.buf.size());
-  hipStream_t st = (hipStream_t)stream;
-  if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), st)) return rc;
+  pl.off_po = mt.size();
+  pl.off_pml = align_up(pl.off_po + (size_t)dp.n_parts * dq * 4, 256);
+  pl.ws_need = align_up(pl.off_pml + (size_t)dp.n_parts * c.n_q_heads * 2 * 4, 256);
+  if (ps_status rc = check_ws(ws, ws_bytes, pl.ws_need)) return rc;
+  pl.ws = ws;
+  pl.gen = kv->meta.generation();
+  pl.n_seqs = n_seqs;
+  pl.n_items = (int32_t)dp.items.size();
+  if (n_seqs > 0) {
+    void* host;
+    const int slot = kv->staging.acquire(mt.size(), &host);
+    if (slot < 0) return PS_E_HIP;
+    std::memcpy(host, mt.buf.data(), mt.buf.size());
+    if (ps_status rc = kv->staging.submit(slot, ws, mt.buf.size(), (hipStream_t)stream)) return rc;
+  }
+  kv->dplan = pl;
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  const DecodeAttnPlan& pl = kv->dplan;
+  if (!pl.ws) return fail(PS_E_INVALID, "no decode attention plan on this handle");
+  if (ws != pl.ws) return fail(PS_E_INVALID, "workspace differs from the planned one");
+  if (pl.gen != kv->meta.generation())
+    return fail(PS_E_INVALID, "the KV pool changed since the decode attention plan was made");
+  if (ps_status rc = check_ws(ws, ws_bytes, pl.ws_need)) return rc;
+  if (pl.n_seqs == 0) return PS_OK;
+  if (!q || !o) return fail(PS_E_INVALID, "null pointer");
+  const ps_layer_cfg& c = kv->cfg;
   char* W = (char*)ws;
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
-  int bad = launch_decode_attn(group_of(c), (int)dp.items.size(), c.n_kv_heads, n_seqs, q, kv->layer_base(layer),
-                               (const SeqInfo*)(W + o_si), (const int32_t*)(W + o_bt),
-                               (const DecodeItem*)(W + o_di), (float*)(W + off_po), (float*)(W + off_pml),
-                               (const int32_t*)(W + o_pb), (const int32_t*)(W + o_pc), o, scale_log2, st);
+  int bad = launch_decode_attn(group_of(c), pl.n_items, c.n_kv_heads, pl.n_seqs, q, kv->layer_base(layer),
+                               (const SeqInfo*)(W + pl.o_si), (const int32_t*)(W + pl.o_bt),
+                               (const DecodeItem*)(W + pl.o_di), (float*)(W + pl.off_po), (float*)(W + pl.off_pml),
+                               (const int32_t*)(W + pl.o_pb), (const int32_t*)(W + pl.o_pc), o, scale_log2,
+                               (hipStream_t)stream);
   if (bad) return fail(PS_E_UNSUPPORTED, "decode attention configuration not supported");
   return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                                            const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
+                                            void* stream) {
+  PS_TRY CHECK_KV(kv);
+  if (ps_status rc = check_layer(kv, layer)) return rc;
+  if (n_seqs > 0 && (!q || !o)) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = ps_op_decode_plan(kv, n_seqs, seqs, split_pages, ws, ws_bytes, stream)) return rc;
+  return ps_op_decode_run(kv, layer, q, o, ws, ws_bytes, stream);
   PS_CATCH
 }

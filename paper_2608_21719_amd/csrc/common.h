@@ -15,6 +15,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kPageTokens = 16;
 constexpr int kGateUpBlock = 32;
+constexpr long kMaxDecodeItems = 65535;  // decode attention work items per launch (grid y)
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }

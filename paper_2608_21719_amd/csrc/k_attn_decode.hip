@@ -4,8 +4,13 @@
 // four waves walk the range's 16-token pages in logical order (wave w takes
 // pages w, w+4, ...), so the arithmetic never depends on where pages sit
 // physically. Per page a wave reads the 4 KiB key block with 16-byte loads
-// and the 4 KiB V^T block with 8-byte loads and does all of the group's
-// query heads at once on the matrix cores:
+// and the 4 KiB V^T block with 8-byte loads, non-temporal (KV is streamed
+// once per step), keeping kPrefetch pages in flight beyond the one it works
+// on; the block table is read with scalar loads, so fetching the next page
+// id never waits on the vector loads already in flight. The kv head is the
+// fastest grid index: workgroups running together read the adjacent heads
+// of the same pages. Each page does all of the group's query heads at once
+// on the matrix cores:
 //
 //   S^T[tok, head] = K[tok, :] . q[head, :]     4 x v_mfma_f32_16x16x32_bf16
 //   O[head, dim]  += P[head, tok] V[tok, dim]   8 x v_mfma_f32_16x16x16_bf16
@@ -25,7 +30,10 @@
 
 namespace ps {
 
-constexpr int kHd = 128;  // head_dim of the MFMA path
+constexpr int kHd = 128;      // head_dim of the MFMA path
+constexpr int kPrefetch = 2;  // pages in flight per wave beyond the current one
+
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 template <int G>
 __global__ __launch_bounds__(256) void decode_attn_kernel(
@@ -33,12 +41,15 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
     const int32_t* __restrict__ bt, const DecodeItem* __restrict__ items, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_kv, float scale_log2) {
   static_assert(G <= 16, "one 16-row MFMA tile per KV group");
-  const int kvh = blockIdx.y;
-  const DecodeItem it = items[blockIdx.x];
+  constexpr int D = kPrefetch;
+  const int kvh = blockIdx.x;
+  const DecodeItem it = items[blockIdx.y];
   const SeqInfo s = si[it.b];
   const int kv_len = s.kv_before + s.n_new;
   const int n_q = n_kv * G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // wave index made wave-uniform so page ids and page addresses stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
 
   // Q operand (B of the S^T product): lane holds q[head c][32j + 8g .. +8].
@@ -59,23 +70,31 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
 
   const int32_t* btr = bt + s.bt_off;
   const int last_page = (kv_len - 1) / kPageTokens;
+  const int koff = c * kHd + 8 * g;                               // + 32 j
+  const int voff = kPageTokens * kHd + c * kPageTokens + 4 * g;   // + 16 blk kPageTokens
+  const long head_off = (long)kvh * (2L * kPageTokens * kHd);
+  const long page_stride = (long)n_kv * (2L * kPageTokens * kHd);
 
-  uint4 kr[4], kn[4];
-  uint2 vr[8], vn[8];
-  auto load_page = [&](int p, uint4* kk, uint2* vv) {
-    const bf16_t* base = pool + ((long)btr[p] * n_kv + kvh) * (2L * kPageTokens * kHd);
+  // ring of page registers: slot 0 is the page being worked on
+  uint4 kr[D + 1][4];
+  uint2 vr[D + 1][8];
+  auto load_page = [&](int p, int slot) {
+    const bf16_t* base = pool + (long)btr[p] * page_stride + head_off;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) kk[j] = *(const uint4*)(base + c * kHd + 32 * j + 8 * g);
-    const bf16_t* vb = base + kPageTokens * kHd + 4 * g;
+    for (int j = 0; j < 4; ++j)
+      kr[slot][j] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const u32x4_t*)(base + koff + 32 * j)));
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) vv[blk] = *(const uint2*)(vb + (16 * blk + c) * kPageTokens);
+    for (int blk = 0; blk < 8; ++blk)
+      vr[slot][blk] = __builtin_bit_cast(
+          uint2, __builtin_nontemporal_load((const u32x2_t*)(base + voff + 16 * blk * kPageTokens)));
   };
 
-  int p = it.page_begin + wave;
-  if (p < it.page_end) load_page(p, kr, vr);
-  for (; p < it.page_end; p += 4) {
-    const int pn = p + 4;
-    if (pn < it.page_end) load_page(pn, kn, vn);
+  const int p0 = it.page_begin + wave;
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (p0 + 4 * d < it.page_end) load_page(p0 + 4 * d, d);
+  for (int p = p0; p < it.page_end; p += 4) {
+    if (p + 4 * D < it.page_end) load_page(p + 4 * D, D);
 
     // tokens past the written length (last page only) hold stale memory:
     // zero their V so 0 * garbage cannot produce NaN
@@ -83,19 +102,19 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
       const int valid = kv_len - p * kPageTokens;  // 1..16
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk) {
-        uint32_t lo = vr[blk].x, hi = vr[blk].y;
+        uint32_t lo = vr[0][blk].x, hi = vr[0][blk].y;
         if (4 * g + 0 >= valid) lo &= 0xffff0000u;
         if (4 * g + 1 >= valid) lo &= 0x0000ffffu;
         if (4 * g + 2 >= valid) hi &= 0xffff0000u;
         if (4 * g + 3 >= valid) hi &= 0x0000ffffu;
-        vr[blk] = make_uint2(lo, hi);
+        vr[0][blk] = make_uint2(lo, hi);
       }
     }
 
     f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[j]), qb[j], st, 0, 0, 0);
+      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[0][j]), qb[j], st, 0, 0, 0);
     // st[r] = score(token 4g + r, head c)
     float sc[4];
     float mx = -INFINITY;
@@ -129,12 +148,16 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
     const s16x4_t pa = __builtin_bit_cast(s16x4_t, make_uint2(pk[0], pk[1]));
 #pragma unroll
     for (int blk = 0; blk < 8; ++blk)
-      acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, __builtin_bit_cast(s16x4_t, vr[blk]), acc[blk],
+      acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, __builtin_bit_cast(s16x4_t, vr[0][blk]), acc[blk],
                                                            0, 0, 0);
+    // advance the ring
 #pragma unroll
-    for (int j = 0; j < 4; ++j) kr[j] = kn[j];
+    for (int d = 0; d < D; ++d) {
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) vr[blk] = vn[blk];
+      for (int j = 0; j < 4; ++j) kr[d][j] = kr[d + 1][j];
+#pragma unroll
+      for (int blk = 0; blk < 8; ++blk) vr[d][blk] = vr[d + 1][blk];
+    }
   }
   // per-head normaliser: sum the four lane groups
   l += __shfl_xor(l, 16);
@@ -200,7 +223,8 @@ int launch_decode_attn(int G, int n_items, int n_kv, int n_seqs, const void* q, 
                        float* part_ml, const int32_t* part_begin, const int32_t* part_count, void* o,
                        float scale_log2, hipStream_t st) {
   if (n_seqs == 0) return 0;
-  dim3 grid(n_items, n_kv);
+  if (n_items > kMaxDecodeItems) return -1;
+  dim3 grid(n_kv, n_items);
   switch (G) {
     case 1: hipLaunchKernelGGL(decode_attn_kernel<1>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
     case 2: hipLaunchKernelGGL(decode_attn_kernel<2>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;

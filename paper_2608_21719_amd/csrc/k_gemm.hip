@@ -247,92 +247,158 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 }
 
 // ==================================================================== skinny
+// Decode-sized M (<= 64): the weight stream is the whole cost (AI = M
+// FLOP/byte). A workgroup owns 64 WN weight rows (output columns) and a K
+// range; its four waves own 16 WN rows each. Stages of 64 k hold the
+// activation tile [16 MB rows][64] and the weight tile [64 WN rows][64];
+// both are filled by global->LDS DMA into an NS-deep ring, so the bytes in
+// flight cost no registers, and one barrier per stage recycles the slot.
+// LDS rows are 128 B with 16-byte chunks XOR-swizzled by row % 8 (the DMA
+// lane order is chosen so the fill lands swizzled). Per 32-wide k step a
+// wave does MB x WN v_mfma_f32_16x16x32_bf16 with A = activations, B = W.
+// With one K split the epilogue is applied from registers; otherwise fp32
+// partials go to the workspace and gemm_reduce_kernel sums them in split
+// order.
 namespace skinny {
 constexpr int NT = 256;
-constexpr int BN = 64;        // columns per workgroup (16 per wave)
-constexpr int KCH = 256;      // K chunk staged per step
+constexpr int KS = 64;    // k per stage
+constexpr int NS = 3;     // ring depth
 constexpr int MAXM = 64;
-// swizzled [64 rows][256] bf16 chunk: 32 16-byte chunks per row
-__device__ __forceinline__ int swz(int row, int ch) { return row * KCH + ((ch ^ (row & 31)) << 3); }
+template <int MB, int WN>
+constexpr size_t lds_bytes() { return (size_t)NS * (16 * MB + 64 * WN) * KS * 2; }
 }  // namespace skinny
 
-template <int MB>
+template <int MB, int WN, int EPI, typename TR, typename TC, bool DIRECT>
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
-                                                          float* __restrict__ part, int M, int N, int K,
-                                                          int k_per_split) {
+                                                          float* __restrict__ part, const TR* __restrict__ R,
+                                                          TC* __restrict__ C, int M, int N, int K, int kps) {
   using namespace skinny;
-  __shared__ __attribute__((aligned(16))) bf16_t sA[2][MB * 16 * KCH];
-  const int n0 = blockIdx.x * BN;
+  static_assert(!(DIRECT && EPI == 2) || WN == 2, "in-kernel SwiGLU pairs a gate and an up block per wave");
+  constexpr int AROWS = 16 * MB, WROWS = 64 * WN;
+  constexpr int STAGE = (AROWS + WROWS) * KS;  // bf16 elements
+  constexpr int TA = AROWS / 8;                // A DMA instructions per stage (8 rows each), round-robin
+  constexpr int WI = WROWS / 8 / 4;            // W DMA instructions per wave per stage
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  const int n0 = blockIdx.x * WROWS;
   const int split = blockIdx.y;
-  const int kb = split * k_per_split;
-  const int nch = k_per_split / KCH;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int kb = split * kps;
+  const int T = kps / KS;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
-  const int col = n0 + wave * 16 + c;
-  const bf16_t* wrow = W + (long)col * K + 8 * g;
-
-  constexpr int AL = MB * 16 * KCH / 8 / NT;  // 16-byte A loads per thread per chunk
-  uint4 ra[AL];
-  auto aload = [&](int k0) {
+  // DMA lane mapping: an instruction fills 8 rows; lane l lands in row l/8 at
+  // chunk l%8, which holds global chunk (l%8) ^ (row%8)
+  const int drow = lane >> 3, dch = (lane & 7) ^ (lane >> 3);
+  const int n_ai = (TA - wave + 3) / 4;  // this wave's A instructions (0..2)
+  const bf16_t* asrc[2];
 #pragma unroll
-    for (int i = 0; i < AL; ++i) {
-      const int id = i * NT + t, row = id >> 5, ch = id & 31;
-      ra[i] = (row < M) ? *(const uint4*)(A + (long)row * K + k0 + ch * 8) : make_uint4(0, 0, 0, 0);
+  for (int i = 0; i < 2; ++i) {
+    const int row = (wave + 4 * i) * 8 + drow;
+    asrc[i] = A + (long)min(row, M - 1) * K + kb + dch * 8;
+  }
+  const bf16_t* wsrc[WI];
+#pragma unroll
+  for (int i = 0; i < WI; ++i) wsrc[i] = W + (long)(n0 + (wave * WI + i) * 8 + drow) * K + kb + dch * 8;
+  auto dma = [&](int t, int slot) {
+    bf16_t* st = smem + slot * STAGE;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      if (i < n_ai) load_lds16(asrc[i] + t * KS, st + (wave + 4 * i) * 8 * KS);
+#pragma unroll
+    for (int i = 0; i < WI; ++i) load_lds16(wsrc[i] + t * KS, st + AROWS * KS + (wave * WI + i) * 8 * KS);
+  };
+  // this wave's own fills older than the most recent stage have landed
+  auto wait_prev_stage = [&]() {
+    if (n_ai == 2) wait_vmcnt_lgkm0<(NS - 2) * (WI + 2)>();
+    else if (n_ai == 1) wait_vmcnt_lgkm0<(NS - 2) * (WI + 1)>();
+    else wait_vmcnt_lgkm0<(NS - 2) * WI>();
+  };
+  auto swz = [](int row, int ch) { return row * KS + ((ch ^ (row & 7)) << 3); };
+  // weight rows of n-block nb for this wave; for SwiGLU (WN 2) block 0 is a
+  // gate block and block 1 the matching up block of the 32-row interleave
+  auto wrow = [&](int nb) {
+    if constexpr (EPI == 2 && WN == 2) {
+      const int q = wave >> 1, h = wave & 1;
+      return 64 * q + 32 * nb + 16 * h + c;
+    } else {
+      return wave * 16 * WN + nb * 16 + c;
     }
   };
-  auto astore = [&](int buf) {
+  f32x4_t acc[WN][MB];
 #pragma unroll
-    for (int i = 0; i < AL; ++i) {
-      const int id = i * NT + t, row = id >> 5, ch = id & 31;
-      *(uint4*)(&sA[buf][swz(row, ch)]) = ra[i];
-    }
-  };
-  u32x4_t wc[KCH / 32], wn[KCH / 32];
-  auto wload = [&](int k0, u32x4_t* w) {
+  for (int nb = 0; nb < WN; ++nb)
 #pragma unroll
-    for (int j = 0; j < KCH / 32; ++j) w[j] = __builtin_nontemporal_load((const u32x4_t*)(wrow + k0 + 32 * j));
-  };
-
-  f32x4_t acc[MB];
+    for (int i = 0; i < MB; ++i) acc[nb][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int slot) {
+    const bf16_t* st = smem + slot * STAGE;
+    const bf16_t* wt = st + AROWS * KS;
 #pragma unroll
-  for (int i = 0; i < MB; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  wload(kb, wc);
-  aload(kb);
-  astore(0);
-  __syncthreads();
-  for (int ci = 0; ci < nch; ++ci) {
-    const int buf = ci & 1;
-    const int knext = kb + (ci + 1) * KCH;
-    if (ci + 1 < nch) {
-      wload(knext, wn);
-      aload(knext);
-    }
+    for (int j = 0; j < 2; ++j) {
+      bf16x8_t wf[WN];
 #pragma unroll
-    for (int j = 0; j < KCH / 32; ++j) {
-      const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wc[j]);
+      for (int nb = 0; nb < WN; ++nb) wf[nb] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(wt + swz(wrow(nb), 4 * j + g)));
 #pragma unroll
       for (int i = 0; i < MB; ++i) {
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sA[buf][swz(16 * i + c, 4 * j + g)]));
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bw, acc[i], 0, 0, 0);
+        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, *(const uint4*)(st + swz(16 * i + c, 4 * j + g)));
+#pragma unroll
+        for (int nb = 0; nb < WN; ++nb)
+          acc[nb][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[nb], acc[nb][i], 0, 0, 0);
       }
     }
-    if (ci + 1 < nch) {
-      astore(buf ^ 1);
+  };
 #pragma unroll
-      for (int j = 0; j < KCH / 32; ++j) wc[j] = wn[j];
-    }
-    __syncthreads();
+  for (int d = 0; d < NS - 1; ++d)
+    if (d < T) dma(d, d);
+  int slot = 0, fill = NS - 1, t = 0;
+  // steady state: every stage refills the slot freed by the previous one
+  for (; t + NS - 1 < T; ++t) {
+    wait_prev_stage();
+    lds_barrier();
+    dma(t + NS - 1, fill);
+    compute(slot);
+    if (++slot == NS) slot = 0;
+    if (++fill == NS) fill = 0;
   }
-  // acc[i][r] = partial C[16i + 4g + r][col]
-  float* pp = part + (long)split * M * N;
+  for (; t < T; ++t) {  // drain
+    wait_vmcnt_lgkm0<0>();
+    lds_barrier();
+    compute(slot);
+    if (++slot == NS) slot = 0;
+  }
+  // acc[nb][i][r] = C[16i + 4g + r][n0 + wrow(nb)]
+  if constexpr (DIRECT) {
 #pragma unroll
-  for (int i = 0; i < MB; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 16 * i + 4 * g + r;
-      if (row < M) pp[(long)row * N + col] = acc[i][r];
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * i + 4 * g + r;
+        if (row >= M) continue;
+        if constexpr (EPI == 2) {
+          const int q = wave >> 1, h = wave & 1;
+          const int col = n0 / 2 + 32 * q + 16 * h + c;
+          st_elt<TC>(C, (long)row * (N / 2) + col, silu_f(acc[0][i][r]) * acc[1][i][r]);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < WN; ++nb) {
+            const long idx = (long)row * N + n0 + wrow(nb);
+            float v = acc[nb][i][r];
+            if constexpr (EPI == 1) v += ld_elt<TR>(R, idx);
+            st_elt<TC>(C, idx, v);
+          }
+        }
+      }
+  } else {
+    float* pp = part + (long)split * M * N;
+#pragma unroll
+    for (int nb = 0; nb < WN; ++nb)
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = 16 * i + 4 * g + r;
+          if (row < M) pp[(long)row * N + n0 + wrow(nb)] = acc[nb][i][r];
+        }
+  }
 }
 
 // Sum split partials in split order, then apply the epilogue.
@@ -472,26 +538,48 @@ static int launch_reduce(int M, int N, int S, const float* part, const void* R, 
 int gemm_skinny_splits(int M, int N, int K) {
   using namespace skinny;
   (void)M;
-  const int tiles = N / BN;
+  const int tiles = N / 64;
   int S = 1;
-  // enough workgroups to keep 256 CUs streaming, K chunks of KCH per split
-  while (tiles * S < 512 && (K % (KCH * S * 2)) == 0 && K / (S * 2) >= 2 * KCH) S *= 2;
+  // at least one workgroup per CU, each split at least four stages long
+  while (tiles * S < 256 && (K % (KS * S * 2)) == 0 && K / (S * 2) >= 4 * KS) S *= 2;
   return S;
 }
 
-static int launch_skinny_core(int M, int N, int K, int S, const void* A, const void* W, float* part, hipStream_t st) {
-  using namespace skinny;
-  dim3 grid(N / BN, S);
-  const int kps = K / S;
-  const int MB = (M + 15) / 16;
-  switch (MB) {
-    case 1: hipLaunchKernelGGL(gemm_skinny_kernel<1>, grid, dim3(NT), 0, st, (const bf16_t*)A, (const bf16_t*)W, part, M, N, K, kps); break;
-    case 2: hipLaunchKernelGGL(gemm_skinny_kernel<2>, grid, dim3(NT), 0, st, (const bf16_t*)A, (const bf16_t*)W, part, M, N, K, kps); break;
-    case 3: hipLaunchKernelGGL(gemm_skinny_kernel<3>, grid, dim3(NT), 0, st, (const bf16_t*)A, (const bf16_t*)W, part, M, N, K, kps); break;
-    case 4: hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, dim3(NT), 0, st, (const bf16_t*)A, (const bf16_t*)W, part, M, N, K, kps); break;
+template <int MB, int WN, int EPI, typename TR, typename TC, bool DIRECT>
+static int launch_skinny_k(int M, int N, int K, int S, const void* A, const void* W, float* part, const void* R,
+                           void* C, hipStream_t st) {
+  constexpr size_t lds = skinny::lds_bytes<MB, WN>();
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)gemm_skinny_kernel<MB, WN, EPI, TR, TC, DIRECT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return -1;
+  hipLaunchKernelGGL((gemm_skinny_kernel<MB, WN, EPI, TR, TC, DIRECT>), dim3(N / (64 * WN), S), dim3(skinny::NT), lds,
+                     st, (const bf16_t*)A, (const bf16_t*)W, part, (const TR*)R, (TC*)C, M, N, K, K / S);
+  return 0;
+}
+
+template <int MB, int EPI, typename TR, typename TC>
+static int launch_skinny_mb(int M, int N, int K, int S, const void* A, const void* W, float* part, const void* R,
+                            void* C, hipStream_t st) {
+  if constexpr (EPI != 2) {
+    if (S == 1) return launch_skinny_k<MB, 1, EPI, TR, TC, true>(M, N, K, 1, A, W, part, R, C, st);
+  } else {
+    if (S == 1 && N % 128 == 0) return launch_skinny_k<MB, 2, 2, TR, TC, true>(M, N, K, 1, A, W, part, R, C, st);
+  }
+  if (launch_skinny_k<MB, 1, EPI, TR, TC, false>(M, N, K, S, A, W, part, R, C, st)) return -1;
+  return launch_reduce<EPI, TR, TC>(M, N, S, part, R, C, st);
+}
+
+template <int EPI, typename TR, typename TC>
+static int launch_skinny(int M, int N, int K, const void* A, const void* W, float* part, const void* R, void* C,
+                         hipStream_t st) {
+  const int S = gemm_skinny_splits(M, N, K);
+  switch ((M + 15) / 16) {
+    case 1: return launch_skinny_mb<1, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
+    case 2: return launch_skinny_mb<2, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
+    case 3: return launch_skinny_mb<3, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
+    case 4: return launch_skinny_mb<4, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
     default: return -1;
   }
-  return 0;
 }
 
 template <int EPI, typename TR, typename TC>
@@ -524,25 +612,23 @@ int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, con
     return -1;
   }
   if (K % 64 != 0) return -1;
-  if (M <= skinny::MAXM && N % skinny::BN == 0 && K % skinny::KCH == 0) {
-    const int S = gemm_skinny_splits(M, N, K);
-    if (ws_bytes < (size_t)S * M * N * sizeof(float)) return -2;
+  if (M <= skinny::MAXM && N % 64 == 0) {
+    if (ws_bytes < gemm_workspace_bytes(dtype, M, N, K)) return -2;
     float* part = (float*)ws;
-    if (launch_skinny_core(M, N, K, S, A, W, part, st)) return -1;
-#define RED_CASE(E, TR_, TC_, rd, cd) \
-  if (epi == E && r_dt == rd && c_dt == cd) return launch_reduce<E, TR_, TC_>(M, N, S, part, R, C, st);
-    RED_CASE(0, float, bf16_t, 0, 1)
-    RED_CASE(0, float, bf16_t, 1, 1)
-    RED_CASE(0, float, float, 0, 0)
-    RED_CASE(0, float, float, 1, 0)
-    RED_CASE(1, bf16_t, float, 1, 0)
-    RED_CASE(1, float, bf16_t, 0, 1)
-    RED_CASE(1, bf16_t, bf16_t, 1, 1)
-    RED_CASE(1, float, float, 0, 0)
-    RED_CASE(2, float, bf16_t, 0, 1)
-    RED_CASE(2, float, bf16_t, 1, 1)
-    RED_CASE(2, float, float, 0, 0)
-#undef RED_CASE
+#define SK_CASE(E, TR_, TC_, rd, cd) \
+  if (epi == E && r_dt == rd && c_dt == cd) return launch_skinny<E, TR_, TC_>(M, N, K, A, W, part, R, C, st);
+    SK_CASE(0, float, bf16_t, 0, 1)
+    SK_CASE(0, float, bf16_t, 1, 1)
+    SK_CASE(0, float, float, 0, 0)
+    SK_CASE(0, float, float, 1, 0)
+    SK_CASE(1, bf16_t, float, 1, 0)
+    SK_CASE(1, float, bf16_t, 0, 1)
+    SK_CASE(1, bf16_t, bf16_t, 1, 1)
+    SK_CASE(1, float, float, 0, 0)
+    SK_CASE(2, float, bf16_t, 0, 1)
+    SK_CASE(2, float, bf16_t, 1, 1)
+    SK_CASE(2, float, float, 0, 0)
+#undef SK_CASE
     return -1;
   }
   if (N % 256 != 0) return -1;
@@ -572,7 +658,7 @@ int gemm_check(int dtype, int epi, int M, int N, int K) {
   if (epi == 2 && N % (2 * kGateUpBlock) != 0) return -1;
   if (dtype == 0) return 0;
   if (dtype != 1 || K % 64 != 0) return -1;
-  if (M <= skinny::MAXM && N % skinny::BN == 0 && K % skinny::KCH == 0) return 0;
+  if (M <= skinny::MAXM && N % 64 == 0) return 0;
   return (N % 256 == 0) ? 0 : -1;
 }
 }  // namespace ps

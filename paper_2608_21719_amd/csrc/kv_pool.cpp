@@ -113,6 +113,7 @@ int KvPool::commit(int32_t n, const int32_t* seqs, const int32_t* n_tok, std::st
       }
   }
   for (int32_t i = 0; i < n; ++i) seqs_[seqs[i]].len += n_tok[i];
+  if (n > 0) ++gen_;
   return PS_OK;
 }
 
@@ -123,6 +124,7 @@ int KvPool::truncate(int32_t s, int32_t new_len, std::string& err) {
     return PS_E_INVALID;
   }
   seqs_[s].len = new_len;
+  ++gen_;
   return PS_OK;
 }
 
@@ -133,6 +135,7 @@ int KvPool::release(int32_t s, std::string& err) {
   q.pages.clear();
   q.len = 0;
   q.open = false;
+  ++gen_;
   return PS_OK;
 }
 

@@ -39,8 +39,12 @@ class KvPool {
   int32_t n_pages() const { return n_pages_; }
   int32_t max_seqs() const { return max_seqs_; }
   int32_t max_pages_per_seq() const { return max_pages_per_seq_; }
+  // bumped by every change to a committed length or a page list that a
+  // planned launch may have captured (commit, truncate, release)
+  uint64_t generation() const { return gen_; }
 
  private:
+  uint64_t gen_ = 0;
   int32_t n_pages_, max_seqs_, max_pages_per_seq_;
   std::vector<int32_t> free_;  // stack: back() is handed out next
   std::vector<KvSeq> seqs_;

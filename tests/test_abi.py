@@ -168,3 +168,27 @@ def test_workspace_and_pool_sizes():
     cfg = B.make_cfg(sh)
     assert B.KV.pool_bytes(cfg, 1, 10) == 10 * 8 * 2 * 16 * 128 * 2
     assert B.Layer.workspace_bytes(cfg, 64, 64, 300) > 64 * (4096 + 14336) * 2
+
+
+def test_decode_run_needs_a_current_plan_and_its_workspace():
+    """Host-side checks of plan/run (no sequences, so nothing is launched)."""
+    from ctypes import c_void_p
+    cfg = B.make_cfg(CONFIGS["llama8b_decode"].shape)
+    kv = B.KV(cfg, 1, 64, 4, 16, FAKE_POOL, 0)
+    ws, ws2, nbytes = c_void_p(0x20000), c_void_p(0x40000), 1 << 20
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_E_INVALID
+    assert B.lib.ps_op_decode_plan(kv.h, 0, None, 0, ws, nbytes, None) == B.PS_OK
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_OK
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws2, nbytes, None) == B.PS_E_INVALID
+    assert B.lib.ps_op_decode_run(kv.h, 1, None, None, ws, nbytes, None) == B.PS_E_INVALID  # layer out of range
+    s = kv.open()
+    kv.alloc(s, 4)
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_OK  # open/alloc keep the plan
+    kv.commit([s], [4])
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_E_INVALID
+    assert "changed" in B.last_error()
+    assert B.lib.ps_op_decode_plan(kv.h, 0, None, 0, ws, nbytes, None) == B.PS_OK
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_OK
+    assert B.lib.ps_op_decode_plan(kv.h, 0, None, -1, ws, nbytes, None) == B.PS_E_INVALID
+    assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_E_INVALID  # failed plan leaves none
+    assert "no decode attention plan" in B.last_error()

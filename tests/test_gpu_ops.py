@@ -314,6 +314,31 @@ def test_decode_attention_ones_v_gives_exactly_one():
     assert np.all(H.to_f64(o) == 1.0)
 
 
+def test_decode_plan_run_matches_one_call_and_detects_pool_change():
+    """Plan once, run for two layers: bit-identical to the one-call op; a
+    commit invalidates the plan."""
+    shape = S8
+    P = H.Pool(shape, 700, 8, 200, n_layers=2, seed=9)
+    seqs, _, _ = fill_kv(P, DEC_LENS, [1] * len(DEC_LENS), "bf16", 100)
+    q = H.to_dev(rnd((len(seqs), shape.n_q, shape.head_dim), "bf16", 52), "bf16")
+    ws = H.workspace(1 << 24)
+    ref = H.empty((len(seqs), shape.d_q), "bf16")
+    B.op_decode_attention(P.kv, 0, seqs, q, ref, ws)
+    B.op_decode_plan(P.kv, seqs, ws)
+    outs = []
+    for layer in (0, 1, 0):
+        o = H.empty((len(seqs), shape.d_q), "bf16")
+        B.op_decode_run(P.kv, layer, q, o, ws)
+        outs.append(o)
+    sync()
+    np.testing.assert_array_equal(H.bits(outs[0]), H.bits(ref))
+    np.testing.assert_array_equal(H.bits(outs[2]), H.bits(ref))
+    P.kv.commit([seqs[0]], [1])
+    with pytest.raises(B.PsError) as e:
+        B.op_decode_run(P.kv, 0, q, H.empty((len(seqs), shape.d_q), "bf16"), ws)
+    assert e.value.code == B.PS_E_INVALID
+
+
 PRE_HIST = [0, 0, 16, 31, 100, 0]
 PRE_NEW = [1, 63, 64, 65, 200, 130]
 
