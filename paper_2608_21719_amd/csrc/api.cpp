@@ -61,6 +61,7 @@ ps_status check_cfg(const ps_layer_cfg* c) {
 struct Staging {
   static constexpr int kSlots = 4;
   void* host[kSlots] = {};
+  void* mapped[kSlots] = {};  // device-side address of host[s]
   size_t cap[kSlots] = {};
   hipEvent_t ev[kSlots] = {};
   bool pending[kSlots] = {};
@@ -86,18 +87,26 @@ struct Staging {
       return (hip_fail(e, "staging event"), -1);
     if (cap[s] < bytes) {
       if (host[s]) (void)hipHostFree(host[s]);
-      host[s] = nullptr;
+      host[s] = mapped[s] = nullptr;
       cap[s] = 0;
       const size_t nb = align_up(std::max<size_t>(bytes, 1 << 16), 1 << 16);
-      if ((e = hipHostMalloc(&host[s], nb, hipHostMallocDefault)) != hipSuccess)
+      // coherent (uncached on the device): the upload kernel reads what the
+      // host wrote just before the launch
+      if ((e = hipHostMalloc(&host[s], nb, hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
         return (hip_fail(e, "staging hipHostMalloc"), -1);
+      if ((e = hipHostGetDevicePointer(&mapped[s], host[s], 0)) != hipSuccess)
+        return (hip_fail(e, "staging device pointer"), -1);
       cap[s] = nb;
     }
     *out = host[s];
     return s;
   }
+  // Copies the slot's first `bytes`, rounded up to 16, to `dev` on `st`
+  // (slots are acquired for the 256-aligned metadata size, and the
+  // destination always has that much room).
   ps_status submit(int s, void* dev, size_t bytes, hipStream_t st) {
-    hipError_t e = hipMemcpyAsync(dev, host[s], bytes, hipMemcpyHostToDevice, st);
+    if (launch_upload(mapped[s], dev, align_up(bytes, 16), st)) return fail(PS_E_INVALID, "metadata upload size");
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "metadata upload");
     if ((e = hipEventRecord(ev[s], st)) != hipSuccess) return hip_fail(e, "staging event record");
     pending[s] = true;

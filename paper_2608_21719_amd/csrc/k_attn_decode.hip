@@ -36,7 +36,7 @@ constexpr int kPrefetch = 2;  // pages in flight per wave beyond the current one
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 template <int G>
-__global__ __launch_bounds__(256) void decode_attn_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_attn_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ pool, const SeqInfo* __restrict__ si,
     const int32_t* __restrict__ bt, const DecodeItem* __restrict__ items, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_kv, float scale_log2) {
@@ -75,46 +75,41 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
   const long head_off = (long)kvh * (2L * kPageTokens * kHd);
   const long page_stride = (long)n_kv * (2L * kPageTokens * kHd);
 
-  // ring of page registers: slot 0 is the page being worked on
-  uint4 kr[D + 1][4];
-  uint2 vr[D + 1][8];
-  auto load_page = [&](int p, int slot) {
+  // three static register sets form the page ring (two pages in flight while
+  // one is consumed); a ring indexed at run time would be copied through
+  // registers, and each copy of an in-flight load waits for it
+  static_assert(kPrefetch == 2, "the page ring below is unrolled for two pages in flight");
+  struct PageRegs {
+    uint4 k[4];
+    uint2 v[8];
+  };
+  PageRegs r0, r1, r2;
+  auto load_page = [&](int p, PageRegs& r) {
     const bf16_t* base = pool + (long)btr[p] * page_stride + head_off;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      kr[slot][j] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const u32x4_t*)(base + koff + 32 * j)));
+      r.k[j] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const u32x4_t*)(base + koff + 32 * j)));
 #pragma unroll
     for (int blk = 0; blk < 8; ++blk)
-      vr[slot][blk] = __builtin_bit_cast(
+      r.v[blk] = __builtin_bit_cast(
           uint2, __builtin_nontemporal_load((const u32x2_t*)(base + voff + 16 * blk * kPageTokens)));
   };
 
-  const int p0 = it.page_begin + wave;
-#pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (p0 + 4 * d < it.page_end) load_page(p0 + 4 * d, d);
-  for (int p = p0; p < it.page_end; p += 4) {
-    if (p + 4 * D < it.page_end) load_page(p + 4 * D, D);
-
+  // consume one page held in `cur`
+  auto page_compute = [&](int p, PageRegs& cur) {
     // tokens past the written length (last page only) hold stale memory:
-    // zero their V so 0 * garbage cannot produce NaN
-    if (p == last_page) {
-      const int valid = kv_len - p * kPageTokens;  // 1..16
+    // zero their V so 0 * garbage cannot produce NaN (branch-free, so no
+    // wait on the page's loads is placed on a path of its own)
+    const int valid = (p == last_page) ? kv_len - p * kPageTokens : kPageTokens;  // 1..16
+    const uint32_t m0 = (4 * g + 0 < valid ? 0x0000ffffu : 0u) | (4 * g + 1 < valid ? 0xffff0000u : 0u);
+    const uint32_t m1 = (4 * g + 2 < valid ? 0x0000ffffu : 0u) | (4 * g + 3 < valid ? 0xffff0000u : 0u);
 #pragma unroll
-      for (int blk = 0; blk < 8; ++blk) {
-        uint32_t lo = vr[0][blk].x, hi = vr[0][blk].y;
-        if (4 * g + 0 >= valid) lo &= 0xffff0000u;
-        if (4 * g + 1 >= valid) lo &= 0x0000ffffu;
-        if (4 * g + 2 >= valid) hi &= 0xffff0000u;
-        if (4 * g + 3 >= valid) hi &= 0x0000ffffu;
-        vr[0][blk] = make_uint2(lo, hi);
-      }
-    }
+    for (int blk = 0; blk < 8; ++blk) cur.v[blk] = make_uint2(cur.v[blk].x & m0, cur.v[blk].y & m1);
 
     f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[0][j]), qb[j], st, 0, 0, 0);
+      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.k[j]), qb[j], st, 0, 0, 0);
     // st[r] = score(token 4g + r, head c)
     float sc[4];
     float mx = -INFINITY;
@@ -148,15 +143,34 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
     const s16x4_t pa = __builtin_bit_cast(s16x4_t, make_uint2(pk[0], pk[1]));
 #pragma unroll
     for (int blk = 0; blk < 8; ++blk)
-      acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, __builtin_bit_cast(s16x4_t, vr[0][blk]), acc[blk],
+      acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, __builtin_bit_cast(s16x4_t, cur.v[blk]), acc[blk],
                                                            0, 0, 0);
-    // advance the ring
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kr[d][j] = kr[d + 1][j];
-#pragma unroll
-      for (int blk = 0; blk < 8; ++blk) vr[d][blk] = vr[d + 1][blk];
+  };
+
+  // wave pages p0, p0 + 4, ...: r0 holds page p and r1 page p + 4 at the top
+  // of every round; a round consumes three pages and requests three
+  const int end = it.page_end;
+  int p = it.page_begin + wave;
+  if (p < end) load_page(p, r0);
+  if (p + 4 < end) load_page(p + 4, r1);
+  for (; p + 16 < end; p += 12) {  // steady state: every request is a real page
+    load_page(p + 8, r2);
+    page_compute(p, r0);
+    load_page(p + 12, r0);
+    page_compute(p + 4, r1);
+    load_page(p + 16, r1);
+    page_compute(p + 8, r2);
+  }
+  if (p < end) {  // at most four pages left: p, p + 4, p + 8, p + 12
+    if (p + 8 < end) load_page(p + 8, r2);
+    page_compute(p, r0);
+    if (p + 4 < end) {
+      if (p + 12 < end) load_page(p + 12, r0);
+      page_compute(p + 4, r1);
+      if (p + 8 < end) {
+        page_compute(p + 8, r2);
+        if (p + 12 < end) page_compute(p + 12, r0);
+      }
     }
   }
   // per-head normaliser: sum the four lane groups

@@ -2,6 +2,8 @@
 #include "common.h"
 #include "launch.h"
 
+#include <algorithm>
+
 namespace ps {
 
 // x[r, :] = table[tokens[r], :], 16 bytes per thread.
@@ -65,6 +67,24 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ l
     // an all-NaN row keeps index 0x7fffffff: clamp to 0 so callers get a valid id
     next[r] = bi == 0x7fffffff ? 0 : bi;
   }
+}
+
+// dst[i] = src[i] for n 16-byte units; src is pinned host memory mapped into
+// the device address space (the per-call metadata upload, done by a kernel
+// rather than a DMA-engine copy because the copy's start-up latency would
+// otherwise sit between the previous call's last kernel and this call's first)
+__global__ __launch_bounds__(256) void upload16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                       long n) {
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) dst[i] = src[i];
+}
+
+int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return 0;
+  if (bytes % 16) return -1;
+  const long n = (long)(bytes / 16);
+  const int blocks = (int)std::min<long>((n + 255) / 256, 64);
+  hipLaunchKernelGGL(upload16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)host_dev_ptr, (uint4*)dst, n);
+  return 0;
 }
 
 int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st) {
