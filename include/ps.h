@@ -31,8 +31,11 @@
  *    pointers are borrowed for the duration of the call.
  *  - Work is enqueued asynchronously on the caller's stream (a hipStream_t
  *    passed as void*; NULL = the null stream). Nothing synchronises
- *    implicitly, except that reuse of a staging slot waits for the copy that
- *    last used it.
+ *    implicitly, except that reuse of a staging slot waits for the upload
+ *    that last used it (a small kernel reading the pinned slot).
+ *  - Device buffers (activations, weights, KV pool, workspace) must be
+ *    16-byte aligned: kernels move them with 16-byte vector accesses.
+ *    Unaligned pointers are rejected with PS_E_INVALID.
  *  - Every function returns ps_status. Arguments, shapes and KV capacity are
  *    validated on the host before anything is enqueued; on any error no work
  *    is enqueued and KV metadata is unchanged. ps_last_error() returns a

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
 #include <vector>
@@ -35,6 +36,13 @@ ps_status fail(ps_status code, const std::string& msg) {
   catch (...) {                                                    \
     return fail(PS_E_INVALID, "internal error");                   \
   }
+
+// Device buffers are accessed with 16-byte vector loads and stores.
+ps_status check_aligned(std::initializer_list<const void*> ptrs) {
+  for (const void* p : ptrs)
+    if ((uintptr_t)p & 15) return fail(PS_E_INVALID, "device buffers must be 16-byte aligned");
+  return PS_OK;
+}
 
 ps_status hip_fail(hipError_t e, const char* what) {
   return fail(PS_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -200,6 +208,7 @@ extern "C" ps_status ps_kv_create(const ps_layer_cfg* c, int32_t n_layers, int32
   if (n_layers <= 0 || n_pages <= 0 || max_seqs <= 0 || max_pages_per_seq <= 0)
     return fail(PS_E_INVALID, "non-positive pool size");
   if (!pool) return fail(PS_E_INVALID, "null pool");
+  if (ps_status rc = check_aligned({pool})) return rc;
   *out = new ps_kv(*c, n_layers, n_pages, max_seqs, max_pages_per_seq, pool, seed);
   return PS_OK;
   PS_CATCH
@@ -451,6 +460,7 @@ size_t meta_bound(const ps_layer_cfg& c, int32_t max_rows, int32_t max_seqs, int
 
 ps_status check_ws(const void* ws, size_t have, size_t need) {
   if (!ws) return fail(PS_E_INVALID, "null workspace");
+  if ((uintptr_t)ws & 15) return fail(PS_E_INVALID, "workspace must be 16-byte aligned");
   if (have < need)
     return fail(PS_E_INVALID, "workspace too small: " + std::to_string(have) + " < " + std::to_string(need));
   return PS_OK;
@@ -478,6 +488,7 @@ extern "C" ps_status ps_kv_append(ps_kv* kv, int32_t layer, int32_t n_seqs, cons
   CallSeqs cs;
   if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
   if (cs.rows > 0 && (!k || !v)) return fail(PS_E_INVALID, "null k or v");
+  if (ps_status rc = check_aligned({k, v})) return rc;
   Meta mt;
   const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
   const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
@@ -504,6 +515,7 @@ extern "C" ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k
   if (int rc = kv->meta.check_open(seq, e)) return fail(rc, e);
   const KvSeq& q = kv->meta.seq(seq);
   if (q.len > 0 && (!k_out || !v_out)) return fail(PS_E_INVALID, "null output");
+  if (ps_status rc = check_aligned({k_out, v_out})) return rc;
   Meta mt;
   const int32_t pages = (q.len + 15) / 16;
   mt.add(q.pages.data(), pages * 4);
@@ -673,7 +685,7 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
 ps_status check_weights(const ps_layer_w* w) {
   if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm || !w->w_gate_up || !w->w_down)
     return fail(PS_E_INVALID, "null weight pointer");
-  return PS_OK;
+  return check_aligned({w->attn_norm, w->w_qkv, w->w_o, w->ffn_norm, w->w_gate_up, w->w_down});
 }
 
 // One layer over n_chunk prefill sequences (chunk_tok rows each) followed by
@@ -692,6 +704,7 @@ ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, 
   if (ps_status rc = plan_layer(c, kv, phase, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, P)) return rc;
   if (P.rows == 0) return PS_OK;
   if (!x_in || !x_out) return fail(PS_E_INVALID, "null activation pointer");
+  if (ps_status rc = check_aligned({x_in, x_out})) return rc;
   P.wl = layout(c, P.mt.size(), P.rows, P.n_parts);
   if (ps_status rc = check_ws(ws, ws_bytes, P.wl.total)) return rc;
   hipStream_t st = (hipStream_t)stream;
@@ -740,6 +753,7 @@ ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, cons
   if (ps_status rc = plan_layer(c, kv, phase, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, P)) return rc;
   if (P.rows == 0) return PS_OK;
   if (!tokens || !next) return fail(PS_E_INVALID, "null token pointer");
+  if (ps_status rc = check_aligned({logits_out})) return rc;
   const int32_t n_out = n_chunk + n_dec;
   if (gemm_check(PS_BF16, PS_EPI_STORE, n_out, M->vocab, c.hidden))
     return fail(PS_E_UNSUPPORTED, "LM head shape not supported by this build");
@@ -791,6 +805,7 @@ extern "C" ps_status ps_model_create(const ps_layer_cfg* c, int32_t n_layers, in
     return fail(PS_E_INVALID, "bad model arguments");
   for (int l = 0; l < n_layers; ++l)
     if (ps_status rc = check_weights(&layers[l])) return rc;
+  if (ps_status rc = check_aligned({embed, final_norm, lm_head})) return rc;
   ps_model* M = new ps_model;
   M->cfg = *c;
   M->n_layers = n_layers;
@@ -880,6 +895,7 @@ extern "C" ps_status ps_op_rmsnorm(int32_t x_dt, int32_t g_dt, int32_t y_dt, int
   PS_TRY
   if (rows < 0 || d <= 0) return fail(PS_E_INVALID, "bad shape");
   if (rows > 0 && (!x || !g || !y)) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({x, g, y})) return rc;
   for (int dt : {x_dt, g_dt, y_dt})
     if (dt != PS_F32 && dt != PS_BF16) return fail(PS_E_INVALID, "bad dtype");
   if (launch_rmsnorm(x_dt, g_dt, y_dt, rows, d, x, g, eps, y, (hipStream_t)stream))
@@ -899,6 +915,7 @@ extern "C" ps_status ps_op_gemm(int32_t dtype, int32_t r_dt, int32_t c_dt, int32
   PS_TRY
   if (epi < 0 || epi > 2) return fail(PS_E_INVALID, "bad epilogue");
   if (M > 0 && (!A || !Wt || !C || (epi == 1 && !R))) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({A, Wt, R, C, ws})) return rc;
   if (gemm_check(dtype, epi, M, N, K)) return fail(PS_E_UNSUPPORTED, "GEMM shape not supported");
   const size_t need = gemm_workspace_bytes(dtype, M, N, K);
   if (need && (!ws || ws_bytes < need)) return fail(PS_E_INVALID, "workspace too small for split-K partials");
@@ -917,6 +934,7 @@ extern "C" ps_status ps_op_rope_kvwrite(ps_kv* kv, int32_t layer, int32_t n_seqs
   CallSeqs cs;
   if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
   if (cs.rows > 0 && (!qkv || !q_out)) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({qkv, q_out})) return rc;
   Meta mt;
   const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
   const size_t o_bt = mt.add(cs.bt.data(), cs.bt.size() * 4);
@@ -947,6 +965,7 @@ extern "C" ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, c
   CallSeqs cs;
   if (ps_status rc = plan_seqs(kv, n_seqs, seqs, n_tok, -1, cs)) return rc;
   if (cs.rows > 0 && (!q || !o)) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({q, o})) return rc;
   const ps_layer_cfg& c = kv->cfg;
   Meta mt;
   const size_t o_si = mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
@@ -1035,6 +1054,7 @@ extern "C" ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, v
   if (ps_status rc = check_ws(ws, ws_bytes, pl.ws_need)) return rc;
   if (pl.n_seqs == 0) return PS_OK;
   if (!q || !o) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({q, o})) return rc;
   const ps_layer_cfg& c = kv->cfg;
   char* W = (char*)ws;
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));

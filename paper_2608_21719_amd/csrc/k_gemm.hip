@@ -17,6 +17,8 @@
 #include "common.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace ps {
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
@@ -79,6 +81,17 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 // collapse a ring deeper than two stages. Callers wait explicitly first; the
 // memory clobber keeps LDS accesses on their side of the barrier.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// bf16 store and SwiGLU epilogues stage the output tile in LDS
+template <int EPI, typename TC>
+constexpr bool staged_epilogue() { return EPI != 1 && std::is_same<TC, bf16_t>::value; }
+template <class CF, int EPI>
+constexpr int tile_out_stride() { return (EPI == 2 ? CF::BN / 2 : CF::BN) * 2 + 16; }
+template <class CF, int EPI, typename TC>
+constexpr size_t tile_lds_bytes() {
+  const size_t staged = staged_epilogue<EPI, TC>() ? (size_t)CF::BM * tile_out_stride<CF, EPI>() : 0;
+  return CF::LDS_BYTES > staged ? CF::LDS_BYTES : staged;
+}
 
 template <class CF, int EPI, typename TR, typename TC>
 __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
@@ -214,7 +227,44 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 
   // epilogue: acc[i][j][r] = C[row 8(r/4) + 4g + r%4][col c] of block (i, j)
   const int rbase = m0 + wm * CF::WTM, cbase = n0 + wn * CF::WTN;
-  if constexpr (EPI == 2) {
+  if constexpr (staged_epilogue<EPI, TC>()) {
+    // bf16 results go through LDS (free after the main loop) so that global
+    // stores are whole 16-byte chunks of full rows rather than 2-byte
+    // scatters; padded rows keep the column writes of rows 4 apart on
+    // different banks
+    constexpr int OCOLS = EPI == 2 ? BN / 2 : BN;
+    constexpr int OSTRIDE = tile_out_stride<CF, EPI>();  // bytes per staged row
+    char* so = (char*)smem;
+    __syncthreads();  // every wave is done reading operand tiles
+#pragma unroll
+    for (int i = 0; i < CF::FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int lrow = wm * CF::WTM + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        if constexpr (EPI == 2) {
+#pragma unroll
+          for (int jp = 0; jp < CF::FN / 2; ++jp) {
+            const int lcol = (wn * CF::WTN >> 1) + jp * 32 + c;
+            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(silu_f(acc[i][2 * jp][r]) * acc[i][2 * jp + 1][r]);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < CF::FN; ++j) {
+            const int lcol = wn * CF::WTN + j * 32 + c;
+            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(acc[i][j][r]);
+          }
+        }
+      }
+    __syncthreads();
+    constexpr int CHUNKS = OCOLS / 8;  // 16-byte chunks per row
+    const long ldc = EPI == 2 ? N / 2 : N;
+    const int ocol0 = EPI == 2 ? n0 / 2 : n0;
+    for (int q = t; q < BM * CHUNKS; q += CF::NT) {
+      const int lrow = q / CHUNKS, ch = q - lrow * CHUNKS;
+      if (m0 + lrow < M)
+        *(uint4*)(C + (long)(m0 + lrow) * ldc + ocol0 + ch * 8) = *(const uint4*)(so + lrow * OSTRIDE + ch * 16);
+    }
+  } else if constexpr (EPI == 2) {
     const int ldc = N / 2;
 #pragma unroll
     for (int i = 0; i < CF::FM; ++i)
@@ -512,11 +562,12 @@ template <class CF, int EPI, typename TR, typename TC>
 int launch_tile_cfg(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
   constexpr int BM = CF::BM, BN = CF::BN;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
+  constexpr size_t lds = tile_lds_bytes<CF, EPI, TC>();
+  static_assert(lds <= 160 * 1024, "LDS per workgroup");
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<CF, EPI, TR, TC>,
-                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                      (int)CF::LDS_BYTES);
+                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return -1;
-  hipLaunchKernelGGL((gemm_tile_kernel<CF, EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(CF::NT), CF::LDS_BYTES, st,
+  hipLaunchKernelGGL((gemm_tile_kernel<CF, EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(CF::NT), lds, st,
                      (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n);
   return 0;
 }

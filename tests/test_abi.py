@@ -192,3 +192,20 @@ def test_decode_run_needs_a_current_plan_and_its_workspace():
     assert B.lib.ps_op_decode_plan(kv.h, 0, None, -1, ws, nbytes, None) == B.PS_E_INVALID
     assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_E_INVALID  # failed plan leaves none
     assert "no decode attention plan" in B.last_error()
+
+
+def test_unaligned_device_pointers_are_rejected_before_launch():
+    """Kernels use 16-byte vector accesses: host-side validation refuses
+    unaligned buffers (nothing is launched, so fake addresses are safe)."""
+    from ctypes import c_void_p
+    ok, bad = c_void_p(0x100000), c_void_p(0x100008)
+    rc = B.lib.ps_op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_STORE, 256, 256, 256, ok, ok, None, bad, ok, 1 << 20,
+                          None)
+    assert rc == B.PS_E_INVALID and "aligned" in B.last_error()
+    rc = B.lib.ps_op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_STORE, 256, 256, 256, ok, ok, None, ok, bad, 1 << 20,
+                          None)
+    assert rc == B.PS_E_INVALID and "aligned" in B.last_error()
+    cfg = B.make_cfg(CONFIGS["tiny_f32"].shape)
+    h = c_void_p()
+    from ctypes import byref
+    assert B.lib.ps_kv_create(byref(cfg), 1, 8, 2, 4, c_void_p(FAKE_POOL + 4), 0, byref(h)) == B.PS_E_INVALID
