@@ -89,7 +89,9 @@ template <class CF, int EPI>
 constexpr int tile_out_stride() { return (EPI == 2 ? CF::BN / 2 : CF::BN) * 2 + 16; }
 template <class CF, int EPI, typename TC>
 constexpr size_t tile_lds_bytes() {
-  const size_t staged = staged_epilogue<EPI, TC>() ? (size_t)CF::BM * tile_out_stride<CF, EPI>() : 0;
+  const size_t staged = staged_epilogue<EPI, TC>() ? (size_t)CF::BM * tile_out_stride<CF, EPI>()
+                        : EPI == 1                ? (size_t)(CF::BM / 2) * (CF::BN * 4 + 32)
+                                                  : 0;
   return CF::LDS_BYTES > staged ? CF::LDS_BYTES : staged;
 }
 
@@ -264,6 +266,53 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
       if (m0 + lrow < M)
         *(uint4*)(C + (long)(m0 + lrow) * ldc + ocol0 + ch * 8) = *(const uint4*)(so + lrow * OSTRIDE + ch * 16);
     }
+  } else if constexpr (EPI == 1) {
+    // residual: the fp32 tile goes through LDS in two halves of 128 rows
+    // (the waves with wm == half write theirs), then every thread adds R and
+    // stores 4 consecutive columns per access; rows of 1056 B put the column
+    // writes of rows 4 apart on opposite bank halves
+    static_assert(CF::WAVES_M == 2 && CF::WTM * 2 == BM, "two row halves of the tile");
+    constexpr int HROWS = BM / 2;
+    constexpr int FSTRIDE = BN * 4 + 32;  // bytes per staged row
+    char* so = (char*)smem;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      __syncthreads();  // operand tiles (first half) or the previous half are no longer read
+      if (wm == half) {
+#pragma unroll
+        for (int i = 0; i < CF::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < CF::FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int lrow = i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+              const int lcol = wn * CF::WTN + j * 32 + c;
+              *(float*)(so + lrow * FSTRIDE + lcol * 4) = acc[i][j][r];
+            }
+      }
+      __syncthreads();
+      constexpr int CHUNKS = BN / 4;  // 4 columns per access
+      for (int q = t; q < HROWS * CHUNKS; q += CF::NT) {
+        const int lrow = q / CHUNKS, ch = q - lrow * CHUNKS;
+        const int row = m0 + half * HROWS + lrow;
+        if (row >= M) continue;
+        const float4 v = *(const float4*)(so + lrow * FSTRIDE + ch * 16);
+        const long idx = (long)row * N + n0 + ch * 4;
+        float o[4] = {v.x, v.y, v.z, v.w};
+        if constexpr (std::is_same<TR, float>::value) {
+          const float4 rr = *(const float4*)(R + idx);
+          o[0] += rr.x; o[1] += rr.y; o[2] += rr.z; o[3] += rr.w;
+        } else {
+          const uint2 rr = *(const uint2*)(R + idx);
+          o[0] += bf_lo(rr.x); o[1] += bf_hi(rr.x); o[2] += bf_lo(rr.y); o[3] += bf_hi(rr.y);
+        }
+        if constexpr (std::is_same<TC, float>::value) {
+          *(float4*)(C + idx) = make_float4(o[0], o[1], o[2], o[3]);
+        } else {
+          *(uint2*)(C + idx) = make_uint2(pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3]));
+        }
+      }
+    }
   } else if constexpr (EPI == 2) {
     const int ldc = N / 2;
 #pragma unroll
@@ -288,9 +337,7 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
           const int row = rbase + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
           if (row < M) {
             const long idx = (long)row * N + cbase + j * 32 + c;
-            float v = acc[i][j][r];
-            if constexpr (EPI == 1) v += ld_elt<TR>(R, idx);
-            st_elt<TC>(C, idx, v);
+            st_elt<TC>(C, idx, acc[i][j][r]);
           }
         }
   }
