@@ -18,6 +18,13 @@
 // of the PV product. The V^T pages (dimension-major) make the A operand a
 // contiguous read. LDS rows are padded (272 B for K, 80 B for V^T) so the
 // 16-byte operand reads of 16 consecutive lanes hit disjoint banks.
+//
+// The pass is bound by the vector ALU (the softmax), not the matrix cores,
+// so the per-score vector work is kept minimal: the running max is taken on
+// raw scores and the scale folds into one FMA per exponent, and the row sum
+// l comes from the matrix cores as a fifth O^T block whose A operand is all
+// ones (so l is the fp32 sum of exactly the bf16 P values the PV product
+// uses, and V == 1 gives exactly 1).
 #include "common.h"
 #include "launch.h"
 
@@ -38,7 +45,7 @@ constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: low
 // tile's products, and written to the other LDS buffer after them, so one
 // barrier per tile suffices and load latency hides behind the MFMAs.
 template <int QB>  // 32-row query blocks per wave; the workgroup's query tile is 32 * QB rows
-__global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restrict__ q,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
                                                          const int32_t* __restrict__ bt,
@@ -84,19 +91,20 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
     for (int kk = 0; kk < 8; ++kk) qf[cb][kk] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * kk));
   }
 
-  f32x16_t oacc[QB][4];
+  // oacc[cb][0..3]: O^T dims 32 db + ...; oacc[cb][4]: every row is l (ones block)
+  f32x16_t oacc[QB][5];
 #pragma unroll
   for (int cb = 0; cb < QB; ++cb)
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+    for (int db = 0; db < 5; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[cb][db][r] = 0.f;
-  float m[QB], l[QB];
+  float m[QB];  // running max of raw (unscaled) scores
 #pragma unroll
-  for (int cb = 0; cb < QB; ++cb) {
-    m[cb] = -INFINITY;
-    l[cb] = 0.f;
-  }
+  for (int cb = 0; cb < QB; ++cb) m[cb] = -INFINITY;
+  bf16x8_t ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
 
   // staging assignment: K chunks (key, 16-byte chunk) e = t, t + 256;
   // V^T halves (page in tile, dim, half) e = t, t + 256
@@ -177,40 +185,31 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
     for (int cb = 0; cb < QB; ++cb) {
       if (!act[cb]) continue;
       const int qpos = qpos0 + 32 * cb + c;
-      float mx = -INFINITY;
-      if (k0 + kKT - 1 <= qpos0 + 32 * cb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sacc[cb][r] *= scale_log2;
-          mx = fmaxf(mx, sacc[cb][r]);
-        }
-      } else {
+      if (k0 + kKT - 1 > qpos0 + 32 * cb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = k0 + 8 * (r >> 2) + 4 * g + (r & 3);
-          sacc[cb][r] = (key <= qpos) ? sacc[cb][r] * scale_log2 : -INFINITY;
-          mx = fmaxf(mx, sacc[cb][r]);
+          if (key > qpos) sacc[cb][r] = -INFINITY;
         }
       }
+      float mx = sacc[cb][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[cb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float m_new = fmaxf(m[cb], mx);  // finite: key 0 is in tile 0
-      float psum = 0.f;
+      const float mb = m_new * scale_log2;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(sacc[cb][2 * i] - m_new),
-                             __builtin_amdgcn_exp2f(sacc[cb][2 * i + 1] - m_new));
-        psum += bf_lo(pk[cb][i]) + bf_hi(pk[cb][i]);
-      }
+      for (int i = 0; i < 8; ++i)
+        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i], scale_log2, -mb)),
+                             __builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i + 1], scale_log2, -mb)));
       // rescale only if some row's running max moved (lane-local factor)
       if (__any(m_new != m[cb])) {
-        const float alpha = __builtin_amdgcn_exp2f(m[cb] - m_new);
-        l[cb] *= alpha;
+        const float alpha = __builtin_amdgcn_exp2f((m[cb] - m_new) * scale_log2);
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+        for (int db = 0; db < 5; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[cb][db][r] *= alpha;
       }
-      l[cb] += psum;
       m[cb] = m_new;
     }
     // O^T += V^T P^T for all row blocks, each V fragment read once
@@ -229,6 +228,9 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
         for (int cb = 0; cb < QB; ++cb)
           if (act[cb]) oacc[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp[cb], oacc[cb][db], 0, 0, 0);
       }
+#pragma unroll
+      for (int cb = 0; cb < QB; ++cb)
+        if (act[cb]) oacc[cb][4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, bp[cb], oacc[cb][4], 0, 0, 0);
     }
     if (kt + 1 < n_tiles) lstore(buf ^ 1);
     __syncthreads();
@@ -239,8 +241,7 @@ __global__ __launch_bounds__(256) void fa_prefill_kernel(const bf16_t* __restric
   for (int cb = 0; cb < QB; ++cb) {
     const int r0 = 32 * cb + c;
     if (r0 >= qn) continue;
-    const float L = l[cb] + __shfl_xor(l[cb], 32);
-    const float inv = 1.f / L;
+    const float inv = 1.f / oacc[cb][4][0];  // l of query c (every row of the ones block)
     bf16_t* op = o + ((long)(s.row_start + it.q_begin + r0) * n_q + head) * kHd;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
