@@ -117,15 +117,20 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
     gemm_tflops = flops / (g_ms * 1e-3) / 1e12
     total_gemm = A.gemm_flops(tokens, sh.hidden, sh.d_q, sh.d_kv, sh.ffn)
     attn = A.prefill_attention_flops([T] * n, sh.n_q, sh.head_dim)
+    # flash attention alone over the K/V the last step wrote (lengths are 0 again)
+    qa = randn(torch, gen, (tokens, sh.n_q, sh.head_dim))
+    oa = torch.empty((tokens, sh.d_q), dtype=torch.bfloat16, device="cuda")
+    a_ms = timer(lambda: B.op_attention(kv, 0, seqs, [T] * n, qa, oa, ws), iters=max(5, steps))
     res = {
         "tok_s": tokens / (ms * 1e-3), "ms_per_step": ms,
         "layer_tflops": (total_gemm + attn) / (ms * 1e-3) / 1e12,
         "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K},
+        "attention": {"ms": a_ms, "tflops": attn / (a_ms * 1e-3) / 1e12},
         "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s",
                                measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
                                ).as_dict(),
     }
-    del pool, ws, tw, x, out, hn, m
+    del pool, ws, tw, x, out, hn, m, qa, oa
     return res
 
 

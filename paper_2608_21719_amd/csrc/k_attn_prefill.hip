@@ -106,27 +106,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
 
-  // staging assignment: K chunks (key, 16-byte chunk) e = t, t + 256;
-  // V^T halves (page in tile, dim, half) e = t, t + 256
+  // staging assignment: load i of thread t covers page i of the tile: K row
+  // t / 16, 16-byte chunk t % 16; V^T dim t / 2, keys 8 (t % 2) .. + 8. The
+  // page ids are workgroup-uniform (scalar), the per-lane offsets fixed.
+  const int koff = (t >> 4) * kHd + (t & 15) * 8;
+  const int voff = kPageTokens * kHd + (t >> 1) * kPageTokens + (t & 1) * 8;
   uint4 rk[2], rv[2];
   auto gload = [&](int k0) {
+    const bool full = k0 + kKT <= kv_valid;  // every key of the tile written
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int e = t + i * NT;
-      const int key = e >> 4, ch = e & 15;
-      const int kpos = k0 + key;
+      const int p0 = k0 + i * kPageTokens;  // first position of page i
       rk[i] = make_uint4(0, 0, 0, 0);
-      if (kpos < kv_valid)
-        rk[i] = *(const uint4*)(pool + page_of(kpos / kPageTokens) * page_stride + kvh_off +
-                                (long)(kpos % kPageTokens) * kHd + ch * 8);
-      const int pt = e / (kHd * 2), rem = e - pt * (kHd * 2);
-      const int dim = rem >> 1, hf = rem & 1;
-      const int pfirst = k0 + pt * kPageTokens;
       rv[i] = make_uint4(0, 0, 0, 0);
-      if (pfirst < kv_valid) {
-        uint4 w = *(const uint4*)(pool + page_of(pfirst / kPageTokens) * page_stride + kvh_off +
-                                  (long)kPageTokens * kHd + (long)dim * kPageTokens + hf * 8);
-        const int valid = kv_valid - pfirst - hf * 8;  // zero keys past the written length
+      if (p0 >= kv_valid) continue;
+      const int pid = __builtin_amdgcn_readfirstlane(page_of(p0 / kPageTokens));
+      const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
+      if (full || p0 + (t >> 4) < kv_valid) rk[i] = *(const uint4*)(base + koff);
+      uint4 w = *(const uint4*)(base + voff);
+      if (!full) {  // zero V^T entries of keys past the written length
+        const int valid = kv_valid - p0 - (t & 1) * 8;
         if (valid < 8) {
           uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -134,20 +133,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
             if (j >= valid) ws[j >> 1] &= (j & 1) ? 0x0000ffffu : 0xffff0000u;
           w = make_uint4(ws[0], ws[1], ws[2], ws[3]);
         }
-        rv[i] = w;
       }
+      rv[i] = w;
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int e = t + i * NT;
-      const int key = e >> 4, ch = e & 15;
-      *(uint4*)(&sK[buf][key * kKRow + ch * 8]) = rk[i];
-      const int pt = e / (kHd * 2), rem = e - pt * (kHd * 2);
-      const int dim = rem >> 1, hf = rem & 1;
+      *(uint4*)(&sK[buf][(16 * i + (t >> 4)) * kKRow + (t & 15) * 8]) = rk[i];
       // half hf = keys 8hf..8hf+7; stored per page as [0-3][8-11][4-7][12-15]
-      bf16_t* dst = &sV[buf][dim * kVRow + pt * kPageTokens];
+      const int dim = t >> 1, hf = t & 1;
+      bf16_t* dst = &sV[buf][dim * kVRow + i * kPageTokens];
       *(uint2*)(dst + hf * 4) = make_uint2(rv[i].x, rv[i].y);
       *(uint2*)(dst + 8 + hf * 4) = make_uint2(rv[i].z, rv[i].w);
     }
