@@ -2,7 +2,7 @@
 // K-contiguous, the nn.Linear layout), fp32 accumulation (gfx950).
 //
 //  * gemm_tile_kernel: prefill-sized M. 256x256x64 workgroup tile, eight
-//    waves of 128x64 (two per SIMD), v_mfma_f32_32x32x16_bf16, operands
+//    waves of 128x64 (two per SIMD), v_mfma_f32_16x16x32_bf16, operands
 //    staged through double-buffered, XOR-swizzled LDS (128 KiB) by direct
 //    global->LDS loads. MFMA-bound.
 //  * gemm_skinny_kernel: decode-sized M (<= 64). Streams W once from HBM
@@ -45,7 +45,7 @@ struct TileCfg {
   static constexpr int NW = WAVES_M * WAVES_N;
   static constexpr int NT = 64 * NW;
   static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
-  static constexpr int FM = WTM / 32, FN = WTN / 32;
+  static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 MFMA blocks per wave
   static constexpr int CPR = BK / 8;               // 16-byte chunks per LDS row
   static constexpr int ROWS_PER_LOAD = 64 / CPR;   // rows one wave instruction fills
   static constexpr int A_ELTS = BM * BK, B_ELTS = BN * BK;
@@ -87,10 +87,12 @@ template <int EPI, typename TC>
 constexpr bool staged_epilogue() { return EPI != 1 && std::is_same<TC, bf16_t>::value; }
 template <class CF, int EPI>
 constexpr int tile_out_stride() { return (EPI == 2 ? CF::BN / 2 : CF::BN) * 2 + 16; }
+template <class CF>
+constexpr int tile_res_stride() { return CF::BN * 4 + 16; }
 template <class CF, int EPI, typename TC>
 constexpr size_t tile_lds_bytes() {
   const size_t staged = staged_epilogue<EPI, TC>() ? (size_t)CF::BM * tile_out_stride<CF, EPI>()
-                        : EPI == 1                ? (size_t)(CF::BM / 2) * (CF::BN * 4 + 32)
+                        : EPI == 1                ? (size_t)(CF::BM / 2) * tile_res_stride<CF>()
                                                   : 0;
   return CF::LDS_BYTES > staged ? CF::LDS_BYTES : staged;
 }
@@ -121,7 +123,7 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int wm = wave / CF::WAVES_N, wn = wave % CF::WAVES_N;
-  const int g = lane >> 5, c = lane & 31;
+  const int g = lane >> 4, c = lane & 15;  // 16x16x32 operand / result lane roles
 
   // per-lane global sources of this wave's loads (row block of the wave)
   const int lrow = lane / CF::CPR, lpos = lane % CF::CPR;
@@ -150,8 +152,9 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
       load_lds16(gb[i] + k0, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
   };
 
-  // operand fragments, double-buffered in registers across 16-wide k steps
-  constexpr int FM = CF::FM, FN = CF::FN, KK = BK / 16;
+  // operand fragments, double-buffered in registers across 32-wide k steps:
+  // lane (g, c) holds row c of a 16-row block, k = 8 g .. 8 g + 7 of the step
+  constexpr int FM = CF::FM, FN = CF::FN, KK = BK / 32;
   static_assert(KK % 2 == 0, "register double-buffering alternates buffers by k-step parity");
   bf16x8_t fa[2][FM], fb[2][FN];
   auto frags = [&](int slot, int kk, int p) {
@@ -159,24 +162,22 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
     const bf16_t* b = a + CF::A_ELTS;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
-      fa[p][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 32 + c, 2 * kk + g)));
+      fa[p][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 16 + c, 4 * kk + g)));
 #pragma unroll
     for (int j = 0; j < FN; ++j)
-      fb[p][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 32 + c, 2 * kk + g)));
+      fb[p][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 16 + c, 4 * kk + g)));
   };
-  f32x16_t acc[FM][FN];
+  f32x4_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   auto mfmas = [&](int p) {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
   };
   // issue order for one k step: the next step's LDS reads spread evenly
   // between this step's MFMAs, so read latency hides under matrix work
@@ -227,12 +228,16 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
     }
   }
 
-  // epilogue: acc[i][j][r] = C[row 8(r/4) + 4g + r%4][col c] of block (i, j)
+  // epilogue: acc[i][j][r] = C[row 16 i + 4 g + r][col 16 j + c] of the wave tile.
+  // SwiGLU pairs: the wave's columns hold 32-row gate/up blocks alternately,
+  // so gate n-block jg = 4 (jp / 2) + jp % 2 pairs with up n-block jg + 2.
   const int rbase = m0 + wm * CF::WTM, cbase = n0 + wn * CF::WTN;
+  auto gate_nb = [](int jp) { return 4 * (jp >> 1) + (jp & 1); };
+  auto gate_col = [](int jp) { return 32 * (jp >> 1) + 16 * (jp & 1); };  // wave-local output column
   if constexpr (staged_epilogue<EPI, TC>()) {
     // bf16 results go through LDS (free after the main loop) so that global
     // stores are whole 16-byte chunks of full rows rather than 2-byte
-    // scatters; padded rows keep the column writes of rows 4 apart on
+    // scatters; padded rows put the four lane groups (rows 4 apart) on
     // different banks
     constexpr int OCOLS = EPI == 2 ? BN / 2 : BN;
     constexpr int OSTRIDE = tile_out_stride<CF, EPI>();  // bytes per staged row
@@ -241,18 +246,19 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 #pragma unroll
     for (int i = 0; i < CF::FM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int lrow = wm * CF::WTM + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+      for (int r = 0; r < 4; ++r) {
+        const int lrow = wm * CF::WTM + i * 16 + 4 * g + r;
         if constexpr (EPI == 2) {
 #pragma unroll
           for (int jp = 0; jp < CF::FN / 2; ++jp) {
-            const int lcol = (wn * CF::WTN >> 1) + jp * 32 + c;
-            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(silu_f(acc[i][2 * jp][r]) * acc[i][2 * jp + 1][r]);
+            const int lcol = (wn * CF::WTN >> 1) + gate_col(jp) + c;
+            const int jg = gate_nb(jp);
+            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(silu_f(acc[i][jg][r]) * acc[i][jg + 2][r]);
           }
         } else {
 #pragma unroll
           for (int j = 0; j < CF::FN; ++j) {
-            const int lcol = wn * CF::WTN + j * 32 + c;
+            const int lcol = wn * CF::WTN + j * 16 + c;
             *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(acc[i][j][r]);
           }
         }
@@ -269,11 +275,11 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
   } else if constexpr (EPI == 1) {
     // residual: the fp32 tile goes through LDS in two halves of 128 rows
     // (the waves with wm == half write theirs), then every thread adds R and
-    // stores 4 consecutive columns per access; rows of 1056 B put the column
-    // writes of rows 4 apart on opposite bank halves
+    // stores 4 consecutive columns per access; rows of 1040 B put the four
+    // lane groups (rows 4 apart) on different banks
     static_assert(CF::WAVES_M == 2 && CF::WTM * 2 == BM, "two row halves of the tile");
     constexpr int HROWS = BM / 2;
-    constexpr int FSTRIDE = BN * 4 + 32;  // bytes per staged row
+    constexpr int FSTRIDE = tile_res_stride<CF>();  // bytes per staged row
     char* so = (char*)smem;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -284,9 +290,9 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 #pragma unroll
           for (int j = 0; j < CF::FN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int lrow = i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-              const int lcol = wn * CF::WTN + j * 32 + c;
+            for (int r = 0; r < 4; ++r) {
+              const int lrow = i * 16 + 4 * g + r;
+              const int lcol = wn * CF::WTN + j * 16 + c;
               *(float*)(so + lrow * FSTRIDE + lcol * 4) = acc[i][j][r];
             }
       }
@@ -320,11 +326,12 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 #pragma unroll
       for (int jp = 0; jp < CF::FN / 2; ++jp)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rbase + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        for (int r = 0; r < 4; ++r) {
+          const int row = rbase + i * 16 + 4 * g + r;
           if (row < M) {
-            const int col = (cbase >> 1) + jp * 32 + c;
-            st_elt<TC>(C, (long)row * ldc + col, silu_f(acc[i][2 * jp][r]) * acc[i][2 * jp + 1][r]);
+            const int jg = gate_nb(jp);
+            const int col = (cbase >> 1) + gate_col(jp) + c;
+            st_elt<TC>(C, (long)row * ldc + col, silu_f(acc[i][jg][r]) * acc[i][jg + 2][r]);
           }
         }
   } else {
@@ -333,12 +340,9 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 #pragma unroll
       for (int j = 0; j < CF::FN; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rbase + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (row < M) {
-            const long idx = (long)row * N + cbase + j * 32 + c;
-            st_elt<TC>(C, idx, acc[i][j][r]);
-          }
+        for (int r = 0; r < 4; ++r) {
+          const int row = rbase + i * 16 + 4 * g + r;
+          if (row < M) st_elt<TC>(C, (long)row * N + cbase + j * 16 + c, acc[i][j][r]);
         }
   }
 }
