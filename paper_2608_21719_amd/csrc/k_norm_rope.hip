@@ -5,6 +5,8 @@
 #include "common.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace ps {
 
 // ---------------------------------------------------------------- RMSNorm
@@ -131,10 +133,28 @@ __device__ __forceinline__ int find_seq(const SeqInfo* __restrict__ si, int n_se
   return lo;
 }
 
+// The same search by one whole wave: each round loads 64 row_starts in
+// parallel and counts those <= row, so n sequences take ceil(log64 n) load
+// round trips instead of log2 n dependent ones. Every lane gets the result.
+__device__ __forceinline__ int find_seq_wave(const SeqInfo* __restrict__ si, int n_seqs, int row) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0, n = n_seqs;
+  while (n > 64) {
+    const int stride = (n + 63) / 64;
+    const int idx = lo + lane * stride;
+    const bool le = idx < lo + n && si[idx].row_start <= row;
+    const int cnt = __popcll(__ballot(le));  // >= 1: si[lo].row_start <= row
+    lo += (cnt - 1) * stride;
+    n = min(stride, n - (cnt - 1) * stride);
+  }
+  const bool le = lane < n && si[lo + lane].row_start <= row;
+  return lo + __popcll(__ballot(le)) - 1;
+}
+
 // ---------------------------------------------------------------- RoPE + KV
 // One row per workgroup: rotate the row's q and k heads (rotate-half, angle
 // pos * inv_freq[j] evaluated in fp64), write q to q_out and k, v into the
-// row's page slot.
+// row's page slot. bf16 rows move four pairs per thread with 8-byte accesses.
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__ qkv, T* __restrict__ q_out,
                                                            T* __restrict__ pool, const SeqInfo* __restrict__ si,
@@ -144,8 +164,13 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   const int row = blockIdx.x;
   const int half = hd >> 1;
   __shared__ float cs[64], sn[64];
-  const int b = find_seq(si, n_seqs, row);
-  const SeqInfo s = si[b];
+  __shared__ int s_b;
+  if (threadIdx.x < 64) {
+    const int b = find_seq_wave(si, n_seqs, row);
+    if (threadIdx.x == 0) s_b = b;
+  }
+  __syncthreads();
+  const SeqInfo s = si[s_b];
   const int pos = s.kv_before + (row - s.row_start);
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
     double a = (double)pos * inv_freq[j];
@@ -159,20 +184,39 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   const T* xr = qkv + (long)row * dqkv;
   const int page = bt[s.bt_off + pos / kPageTokens];
   const int slot = pos % kPageTokens;
-  // q and k: rotate pairs (j, j + half)
-  for (int idx = threadIdx.x; idx < (n_q + n_kv) * half; idx += blockDim.x) {
-    int head = idx / half, j = idx - head * half;
-    float x1 = Elt<T>::load(xr, head * hd + j);
-    float x2 = Elt<T>::load(xr, head * hd + j + half);
-    float y1 = x1 * cs[j] - x2 * sn[j];
-    float y2 = x2 * cs[j] + x1 * sn[j];
-    if (head < n_q) {
-      Elt<T>::store(q_out, (long)row * n_q * hd + head * hd + j, y1);
-      Elt<T>::store(q_out, (long)row * n_q * hd + head * hd + j + half, y2);
-    } else {
-      long base = kv_block(page, head - n_q, n_kv, hd) + (long)slot * hd;
-      Elt<T>::store(pool, base + j, y1);
-      Elt<T>::store(pool, base + j + half, y2);
+  auto dst_of = [&](int head) -> T* {  // start of the head's rotated row
+    return head < n_q ? q_out + (long)row * n_q * hd + head * hd
+                      : pool + kv_block(page, head - n_q, n_kv, hd) + (long)slot * hd;
+  };
+  bool quad = false;
+  if constexpr (std::is_same<T, bf16_t>::value) quad = (half % 4) == 0;
+  if (quad) {
+    // q and k: pairs (j, j + half), four consecutive j per thread (hd % 8 == 0)
+    const int quads = half / 4;
+    for (int idx = threadIdx.x; idx < (n_q + n_kv) * quads; idx += blockDim.x) {
+      const int head = idx / quads, j = (idx - head * quads) * 4;
+      const uint2 a = *(const uint2*)(xr + head * hd + j);
+      const uint2 c = *(const uint2*)(xr + head * hd + j + half);
+      const float x1[4] = {bf_lo(a.x), bf_hi(a.x), bf_lo(a.y), bf_hi(a.y)};
+      const float x2[4] = {bf_lo(c.x), bf_hi(c.x), bf_lo(c.y), bf_hi(c.y)};
+      float y1[4], y2[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y1[e] = x1[e] * cs[j + e] - x2[e] * sn[j + e];
+        y2[e] = x2[e] * cs[j + e] + x1[e] * sn[j + e];
+      }
+      T* d = dst_of(head);
+      *(uint2*)(d + j) = make_uint2(pack_bf2(y1[0], y1[1]), pack_bf2(y1[2], y1[3]));
+      *(uint2*)(d + j + half) = make_uint2(pack_bf2(y2[0], y2[1]), pack_bf2(y2[2], y2[3]));
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < (n_q + n_kv) * half; idx += blockDim.x) {
+      int head = idx / half, j = idx - head * half;
+      float x1 = Elt<T>::load(xr, head * hd + j);
+      float x2 = Elt<T>::load(xr, head * hd + j + half);
+      T* d = dst_of(head);
+      Elt<T>::store(d, j, x1 * cs[j] - x2 * sn[j]);
+      Elt<T>::store(d, j + half, x2 * cs[j] + x1 * sn[j]);
     }
   }
   // v: stored dimension-major within the page
@@ -205,8 +249,13 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const T* __restrict__ k,
                                                         const int32_t* __restrict__ bt, int n_seqs, int n_kv,
                                                         int hd) {
   const int row = blockIdx.x;
-  const int b = find_seq(si, n_seqs, row);
-  const SeqInfo s = si[b];
+  __shared__ int s_b;
+  if (threadIdx.x < 64) {
+    const int b = find_seq_wave(si, n_seqs, row);
+    if (threadIdx.x == 0) s_b = b;
+  }
+  __syncthreads();
+  const SeqInfo s = si[s_b];
   const int pos = s.kv_before + (row - s.row_start);
   const int page = bt[s.bt_off + pos / kPageTokens];
   const int slot = pos % kPageTokens;
