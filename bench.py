@@ -42,13 +42,16 @@ def randn(torch, gen, shape, std=1.0, mean=0.0):
 
 
 def make_layer_weights(torch, B, shape, gen):
+    """Random-init layer weights drawn directly in the library's layouts:
+    entries are iid, so the gate/up row interleave and the 64x64 weight
+    tiling are relabellings of an iid matrix and need no conversion pass."""
     d, dq, dkv, f = shape.hidden, shape.d_q, shape.d_kv, shape.ffn
     t = {
         "attn_norm": randn(torch, gen, (d,), 0.02, 1.0),
         "w_qkv": randn(torch, gen, (dq + 2 * dkv, d), 0.02),
         "w_o": randn(torch, gen, (d, dq), 0.02),
         "ffn_norm": randn(torch, gen, (d,), 0.02, 1.0),
-        "w_gate_up": randn(torch, gen, (2 * f, d), 0.02),  # iid rows: interleaving is a relabelling
+        "w_gate_up": randn(torch, gen, (2 * f, d), 0.02),
         "w_down": randn(torch, gen, (d, f), 0.02),
     }
     return t, B.layer_weights(**t)
@@ -288,7 +291,7 @@ def bench_model70b(torch, B, A, wl, steps, warmup):
         tws.append(tw)
         ws_list.append(w)
     embed = randn(torch, gen, (V, sh.hidden), 0.02)
-    lm_head = randn(torch, gen, (V, sh.hidden), 0.02)
+    lm_head = randn(torch, gen, (V, sh.hidden), 0.02)  # iid: already a valid tiled weight
     final_norm = randn(torch, gen, (sh.hidden,), 0.02, 1.0)
     ctx = wl.ctx_params[0]
     nb, npf, tp = wl.decode_batch, wl.prefill_seqs, wl.prefill_tokens

@@ -41,8 +41,16 @@
  *    is enqueued and KV metadata is unchanged. ps_last_error() returns a
  *    thread-local message for the last failing call on this thread.
  *  - A handle is not thread-safe; distinct handles are independent.
- *  - Matrices are row-major. Linear weights use the W[out, in] convention
- *    (y = x W^T). bf16 buffers hold IEEE bfloat16 bit patterns.
+ *  - Activations and the embedding table are row-major. Linear weights use
+ *    the W[out, in] convention (y = x W^T) and are stored TILED: 64 x 64
+ *    tiles, tile (i, j) = W[64i .. 64i+63, 64j .. 64j+63] at tile index
+ *    i * ceil(in/64) + j, each tile row-major; rows/columns past the edge of
+ *    W are zero. Element W[n, k] is at
+ *      ((n / 64) * ceil(in / 64) + k / 64) * 4096 + (n % 64) * 64 + k % 64.
+ *    ps_tile_weight (host) and ps_op_tile_weight (device) convert a
+ *    row-major matrix. Tiles make every 64-row x 64-column slab a GEMM
+ *    streams one contiguous block of HBM.
+ *  - bf16 buffers hold IEEE bfloat16 bit patterns.
  */
 #ifndef PS_H
 #define PS_H
@@ -84,14 +92,15 @@ typedef struct {
   int32_t dtype;       /* ps_dtype of weights, activations and KV */
 } ps_layer_cfg;
 
-/* One layer's device weights, all in cfg.dtype:
+/* One layer's device weights, all in cfg.dtype; the four matrices are
+ * tiled (see the conventions above):
  *   attn_norm, ffn_norm  [d]
  *   w_qkv      [d_q + 2 d_kv, d]  rows: Wq (head-major), then Wk, then Wv
  *   w_o        [d, d_q]
  *   w_gate_up  [2F, d]  Wg and Wu rows interleaved in blocks of
  *              PS_GATE_UP_BLOCK (= 32) rows: block 2i = Wg rows
  *              [32i, 32i+32), block 2i+1 = Wu rows [32i, 32i+32)
- *              (see ps_pack_gate_up)
+ *              (see ps_pack_gate_up), then tiled
  *   w_down     [d, F]                                                    */
 typedef struct {
   const void *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate_up, *w_down;
@@ -108,6 +117,20 @@ const char* ps_version(void);
  * Pure layout, no arithmetic. F must be a multiple of PS_GATE_UP_BLOCK. */
 ps_status ps_pack_gate_up(const void* wg, const void* wu, int32_t F, int32_t d, int32_t elt_bytes,
                           void* out);
+
+/* Elements of the tiled form of an N x K weight: ceil(N/64) ceil(K/64) 4096
+ * (0 for non-positive sizes). */
+size_t ps_tiled_weight_elems(int32_t N, int32_t K);
+
+/* Host helper: row-major w [N, K] (host memory, elt_bytes = 2 or 4 per
+ * element) -> tiled `out` of ps_tiled_weight_elems(N, K) elements, padding
+ * zeroed. Pure layout, no arithmetic. */
+ps_status ps_tile_weight(const void* w, int32_t N, int32_t K, int32_t elt_bytes, void* out);
+
+/* The same conversion on the device: w and out are device buffers of
+ * dtype (ps_dtype), out of ps_tiled_weight_elems(N, K) elements and not
+ * overlapping w. Enqueued on stream; no arithmetic. */
+ps_status ps_op_tile_weight(int32_t dtype, int32_t N, int32_t K, const void* w, void* out, void* stream);
 
 /* ------------------------------------------------------------------ KV pool
  * Device layout of the caller-provided pool (cfg.dtype elements):
@@ -198,7 +221,8 @@ ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t lay
  * Layer l uses layer l of the KV pool (which needs >= n_layers layers):
  *   h0 = embed[token];  h_L = layer_{L-1}(... layer_0(h0));
  *   logits = RMSNorm(h_L) * g_final · W_lmᵀ;  next = argmax (ties -> lowest id)
- * embed and lm_head are [vocab, d]; final_norm [d]; `layers` is a host array
+ * embed [vocab, d] is row-major, lm_head [vocab, d] tiled; final_norm [d];
+ * `layers` is a host array
  * of n_layers weight sets (device pointers, borrowed until destroy).
  * Token ids live on the device; an id outside [0, vocab) embeds as a zero
  * row. Neither call commits: call ps_kv_commit after it.
@@ -229,8 +253,8 @@ ps_status ps_model_decode_step(ps_model* model, ps_kv* kv, int32_t phase, int32_
 ps_status ps_op_rmsnorm(int32_t x_dtype, int32_t g_dtype, int32_t y_dtype, int32_t rows, int32_t d,
                         const void* x, const void* g, float eps, void* y, void* stream);
 
-/* C = epilogue(A W^T): A [M, K], W [N, K], both `dtype` (bf16 uses the MFMA
- * path, fp32 a vector path), fp32 accumulation.
+/* C = epilogue(A W^T): A [M, K] row-major, W [N, K] tiled, both `dtype`
+ * (bf16 uses the MFMA path, fp32 a vector path), fp32 accumulation.
  *   PS_EPI_STORE     C[M, N] (c_dtype)
  *   PS_EPI_RESIDUAL  C[M, N] = R + A W^T, R of r_dtype (R may alias C when
  *                    the dtypes match)
@@ -238,8 +262,8 @@ ps_status ps_op_rmsnorm(int32_t x_dtype, int32_t g_dtype, int32_t y_dtype, int32
  *                    silu(gate) * up with gate/up the de-interleaved halves
  * Decode-sized M (<= 64) splits K across workgroups and needs ws of at least
  * ps_op_gemm_workspace_bytes for its fp32 partials (0 bytes otherwise).
- * Supported: bf16 with K % 64 == 0 and N % 256 == 0 (or M <= 64,
- * N % 64 == 0, K % 256 == 0); fp32 any shape; SwiGLU needs N % 64 == 0. */
+ * Supported: bf16 with K % 64 == 0 and N % 256 == 0 (or M <= 64 and
+ * N % 64 == 0); fp32 any shape; SwiGLU needs N % 64 == 0. */
 #define PS_EPI_STORE 0
 #define PS_EPI_RESIDUAL 1
 #define PS_EPI_SWIGLU 2

@@ -66,6 +66,9 @@ _SIGS = {
     "ps_last_error": (c_char_p, []),
     "ps_version": (c_char_p, []),
     "ps_pack_gate_up": (_I, [_P, _P, _I, _I, _I, _P]),
+    "ps_tiled_weight_elems": (c_size_t, [_I, _I]),
+    "ps_tile_weight": (_I, [_P, _I, _I, _I, _P]),
+    "ps_op_tile_weight": (_I, [_I, _I, _I, _P, _P, _P]),
     "ps_kv_pool_bytes": (c_size_t, [POINTER(LayerCfg), _I, _I]),
     "ps_kv_create": (_I, [POINTER(LayerCfg), _I, _I, _I, _I, _P, c_uint64, POINTER(c_void_p)]),
     "ps_kv_destroy": (_I, [_P]),
@@ -159,6 +162,26 @@ def pack_gate_up(wg, wu):
     out = np.empty((2 * F, d), dtype=wg.dtype)
     check(lib.ps_pack_gate_up(ptr(wg), ptr(wu), F, d, wg.itemsize, ptr(out)))
     return out
+
+
+def tiled_weight_elems(N: int, K: int) -> int:
+    return lib.ps_tiled_weight_elems(N, K)
+
+
+def tile_weight(w):
+    """Host numpy conversion of a row-major [N, K] weight to the tiled layout
+    (a flat array of tiled_weight_elems(N, K) elements)."""
+    import numpy as np
+    w = np.ascontiguousarray(w)
+    N, K = w.shape
+    out = np.empty(tiled_weight_elems(N, K), dtype=w.dtype)
+    check(lib.ps_tile_weight(ptr(w), N, K, w.itemsize, ptr(out)))
+    return out
+
+
+def op_tile_weight(dtype, N, K, w, out, stream=None):
+    """Device conversion of a row-major [N, K] weight to the tiled layout."""
+    check(lib.ps_op_tile_weight(dtype, N, K, ptr(w), ptr(out), stream_handle(stream)))
 
 
 # ---------------------------------------------------------------- handles

@@ -194,6 +194,28 @@ extern "C" ps_status ps_pack_gate_up(const void* wg, const void* wu, int32_t F, 
   PS_CATCH
 }
 
+extern "C" size_t ps_tiled_weight_elems(int32_t N, int32_t K) {
+  if (N <= 0 || K <= 0) return 0;
+  return (size_t)tiled_weight_elems(N, K);
+}
+
+extern "C" ps_status ps_tile_weight(const void* w, int32_t N, int32_t K, int32_t eb, void* out) {
+  PS_TRY
+  if (!w || !out || N <= 0 || K <= 0 || (eb != 2 && eb != 4)) return fail(PS_E_INVALID, "bad arguments");
+  const long kt = (K + kWTile - 1) / kWTile, nt = (N + kWTile - 1) / kWTile;
+  std::memset(out, 0, (size_t)tiled_weight_elems(N, K) * eb);
+  for (long i = 0; i < nt; ++i)
+    for (long j = 0; j < kt; ++j) {
+      const long cols = std::min<long>(kWTile, K - j * kWTile);
+      char* tile = (char*)out + (size_t)(i * kt + j) * kWTileElts * eb;
+      for (long r = 0; r < kWTile && i * kWTile + r < N; ++r)
+        std::memcpy(tile + (size_t)r * kWTile * eb, (const char*)w + ((size_t)(i * kWTile + r) * K + j * kWTile) * eb,
+                    (size_t)cols * eb);
+    }
+  return PS_OK;
+  PS_CATCH
+}
+
 // ------------------------------------------------------------------ KV pool
 extern "C" size_t ps_kv_pool_bytes(const ps_layer_cfg* c, int32_t n_layers, int32_t n_pages) {
   if (!c || n_layers <= 0 || n_pages <= 0) return 0;
@@ -922,6 +944,17 @@ extern "C" ps_status ps_op_gemm(int32_t dtype, int32_t r_dt, int32_t c_dt, int32
   if (epi != 1) r_dt = 0;
   int rc = launch_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, Wt, R, C, ws, ws_bytes, (hipStream_t)stream);
   if (rc) return fail(PS_E_UNSUPPORTED, "dtype/epilogue combination not supported");
+  return last_launch_error();
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_tile_weight(int32_t dtype, int32_t N, int32_t K, const void* w, void* out, void* stream) {
+  PS_TRY
+  if (!w || !out || N <= 0 || K <= 0 || (dtype != PS_F32 && dtype != PS_BF16))
+    return fail(PS_E_INVALID, "bad arguments");
+  if (ps_status rc = check_aligned({w, out})) return rc;
+  if (launch_tile_weight(elt_bytes(dtype), N, K, w, out, (hipStream_t)stream))
+    return fail(PS_E_UNSUPPORTED, "element size");
   return last_launch_error();
   PS_CATCH
 }

@@ -16,6 +16,17 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kPageTokens = 16;
 constexpr int kGateUpBlock = 32;
 constexpr long kMaxDecodeItems = 65535;  // decode attention work items per launch (grid y)
+// Linear weights W[N, K] are stored in 64x64 tiles (tile (i, j) at index
+// i * ceil(K/64) + j, row-major inside; edge tiles zero-padded).
+constexpr int kWTile = 64;
+constexpr int kWTileElts = kWTile * kWTile;
+__host__ __device__ inline long tiled_weight_elems(long N, long K) {
+  return ((N + kWTile - 1) / kWTile) * ((K + kWTile - 1) / kWTile) * kWTileElts;
+}
+__host__ __device__ inline long tiled_index(long n, long k, long K) {
+  const long kt = (K + kWTile - 1) / kWTile;
+  return ((n / kWTile) * kt + k / kWTile) * kWTileElts + (n % kWTile) * kWTile + (k % kWTile);
+}
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }

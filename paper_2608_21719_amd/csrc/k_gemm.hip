@@ -1,5 +1,9 @@
-// GEMMs of the layer: C = epilogue(A W^T), A [M, K], W [N, K] (both
-// K-contiguous, the nn.Linear layout), fp32 accumulation (gfx950).
+// GEMMs of the layer: C = epilogue(A W^T), A [M, K] row-major, W [N, K]
+// (the nn.Linear orientation) stored in 64x64 tiles: tile (i, j) covers rows
+// 64i.. and columns 64j.., sits at tile index i * ceil(K/64) + j, and is
+// row-major inside (64 rows of 64 elements). Every 64-row by 64-k slab a
+// workgroup streams is then one contiguous 8 KiB (bf16) block of HBM rather
+// than 64 strided 128-byte pieces. fp32 accumulation (gfx950).
 //
 //  * gemm_tile_kernel: prefill-sized M. 256x256x64 workgroup tile, eight
 //    waves of 128x64 (two per SIMD), v_mfma_f32_16x16x32_bf16, operands
@@ -139,17 +143,19 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
   for (int i = 0; i < CF::B_LOADS; ++i) {
     const int row = (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD + lrow;
     const int ch = lpos ^ ((row / (16 / CF::CPR)) % CF::CPR);
-    gb[i] = W + (long)(n0 + row) * K + ch * 8;
+    const int n = n0 + row;  // tiled W: k-tile kt of row n at ((n/64) K/64 + kt) 4096 + (n%64) 64
+    gb[i] = W + (long)(n >> 6) * (K / 64) * kWTileElts + (n & 63) * 64 + ch * 8;
   }
-  auto gload = [&](int k0, int stage) {
+  static_assert(BK == 64, "one W tile per k step");
+  auto gload = [&](int kt, int stage) {
     bf16_t* a = smem + stage * CF::STAGE_ELTS;
     bf16_t* b = a + CF::A_ELTS;
 #pragma unroll
     for (int i = 0; i < CF::A_LOADS; ++i)
-      load_lds16(ga[i] + k0, a + (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD * BK);
+      load_lds16(ga[i] + kt * BK, a + (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD * BK);
 #pragma unroll
     for (int i = 0; i < CF::B_LOADS; ++i)
-      load_lds16(gb[i] + k0, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
+      load_lds16(gb[i] + (long)kt * kWTileElts, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
   };
 
   // operand fragments, double-buffered in registers across 32-wide k steps:
@@ -197,11 +203,11 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
   // stage STAGES-1 issued; fragments of (stage 0, k step 0) requested
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
-    if (st < KT) gload(st * BK, st);
+    if (st < KT) gload(st, st);
   if (STAGES - 2 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
   else wait_vmcnt_lgkm0<0>();
   lds_barrier();
-  if (STAGES - 1 < KT) gload((STAGES - 1) * BK, STAGES - 1);
+  if (STAGES - 1 < KT) gload(STAGES - 1, STAGES - 1);
   frags(0, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
     const int slot = kt % STAGES;
@@ -221,7 +227,7 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
           if (kt + STAGES - 1 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
           else wait_vmcnt_lgkm0<0>();
           lds_barrier();
-          if (kt + STAGES < KT) gload((kt + STAGES) * BK, slot);
+          if (kt + STAGES < KT) gload(kt + STAGES, slot);
           frags((kt + 1) % STAGES, 0, p ^ 1);
         }
       }
@@ -363,7 +369,7 @@ __global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
 namespace skinny {
 constexpr int NT = 256;
 constexpr int KS = 64;    // k per stage
-constexpr int NS = 3;     // ring depth
+constexpr int NS = 4;     // ring depth
 constexpr int MAXM = 64;
 template <int MB, int WN>
 constexpr size_t lds_bytes() { return (size_t)NS * (16 * MB + 64 * WN) * KS * 2; }
@@ -375,6 +381,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
                                                           TC* __restrict__ C, int M, int N, int K, int kps) {
   using namespace skinny;
   static_assert(!(DIRECT && EPI == 2) || WN == 2, "in-kernel SwiGLU pairs a gate and an up block per wave");
+  static_assert(KS == kWTile, "one W tile per stage");
   constexpr int AROWS = 16 * MB, WROWS = 64 * WN;
   constexpr int STAGE = (AROWS + WROWS) * KS;  // bf16 elements
   constexpr int TA = AROWS / 8;                // A DMA instructions per stage (8 rows each), round-robin
@@ -397,16 +404,20 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
     const int row = (wave + 4 * i) * 8 + drow;
     asrc[i] = A + (long)min(row, M - 1) * K + kb + dch * 8;
   }
+  // tiled W: the stage's 64 k of each 64-row block is one contiguous tile
   const bf16_t* wsrc[WI];
 #pragma unroll
-  for (int i = 0; i < WI; ++i) wsrc[i] = W + (long)(n0 + (wave * WI + i) * 8 + drow) * K + kb + dch * 8;
+  for (int i = 0; i < WI; ++i) {
+    const int n = n0 + (wave * WI + i) * 8 + drow;
+    wsrc[i] = W + ((long)(n >> 6) * (K / 64) + kb / 64) * kWTileElts + (n & 63) * 64 + dch * 8;
+  }
   auto dma = [&](int t, int slot) {
     bf16_t* st = smem + slot * STAGE;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       if (i < n_ai) load_lds16(asrc[i] + t * KS, st + (wave + 4 * i) * 8 * KS);
 #pragma unroll
-    for (int i = 0; i < WI; ++i) load_lds16(wsrc[i] + t * KS, st + AROWS * KS + (wave * WI + i) * 8 * KS);
+    for (int i = 0; i < WI; ++i) load_lds16(wsrc[i] + (long)t * kWTileElts, st + AROWS * KS + (wave * WI + i) * 8 * KS);
   };
   // this wave's own fills older than the most recent stage have landed
   auto wait_prev_stage = [&]() {
@@ -542,7 +553,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       const int r = e >> 4, kk = e & 15;
       const int k = k0 + kk;
       sA[kk][r] = (m0 + r < M && k < K) ? A[(long)(m0 + r) * K + k] : 0.f;
-      sW[kk][r] = (n0 + r < N && k < K) ? W[(long)(n0 + r) * K + k] : 0.f;
+      sW[kk][r] = (n0 + r < N && k < K) ? W[tiled_index(n0 + r, k, K)] : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -637,14 +648,28 @@ static int launch_reduce(int M, int N, int S, const float* part, const void* R, 
   return 0;
 }
 
-int gemm_skinny_splits(int M, int N, int K) {
+// Skinny launch plan: WN 64-row blocks per workgroup and S K-splits. Two
+// blocks per workgroup halve the activation traffic per weight byte and win
+// whenever the grid still reaches ~160 workgroups; otherwise one block. The
+// split count doubles until the grid reaches its target, while each split
+// keeps at least 16 stages (shorter splits lose more to ring fill and
+// drain than they gain in parallelism, and add partial-sum traffic).
+// Chosen from a sweep of both widths and 1..8 splits over the 8B and 70B
+// decode shapes at M = 32 and 64, reduction included.
+static int skinny_splits_for(int tiles, int K, int target) {
   using namespace skinny;
-  (void)M;
-  const int tiles = N / 64;
   int S = 1;
-  // at least one workgroup per CU, each split at least four stages long
-  while (tiles * S < 256 && (K % (KS * S * 2)) == 0 && K / (S * 2) >= 4 * KS) S *= 2;
+  while (tiles * S < target && (K % (KS * S * 2)) == 0 && K / (S * 2) >= 16 * KS) S *= 2;
   return S;
+}
+
+SkinnyPlan gemm_skinny_plan(int M, int N, int K) {
+  (void)M;
+  if (N % 128 == 0) {
+    const int S = skinny_splits_for(N / 128, K, 160);
+    if ((N / 128) * S >= 160) return {2, S};
+  }
+  return {1, skinny_splits_for(N / 64, K, 256)};
 }
 
 template <int MB, int WN, int EPI, typename TR, typename TC, bool DIRECT>
@@ -659,29 +684,40 @@ static int launch_skinny_k(int M, int N, int K, int S, const void* A, const void
   return 0;
 }
 
-template <int MB, int EPI, typename TR, typename TC>
-static int launch_skinny_mb(int M, int N, int K, int S, const void* A, const void* W, float* part, const void* R,
+template <int MB, int WN, int EPI, typename TR, typename TC>
+static int launch_skinny_wn(int M, int N, int K, int S, const void* A, const void* W, float* part, const void* R,
                             void* C, hipStream_t st) {
-  if constexpr (EPI != 2) {
-    if (S == 1) return launch_skinny_k<MB, 1, EPI, TR, TC, true>(M, N, K, 1, A, W, part, R, C, st);
-  } else {
-    if (S == 1 && N % 128 == 0) return launch_skinny_k<MB, 2, 2, TR, TC, true>(M, N, K, 1, A, W, part, R, C, st);
+  if constexpr (EPI != 2 || WN == 2) {
+    if (S == 1) return launch_skinny_k<MB, WN, EPI, TR, TC, true>(M, N, K, 1, A, W, part, R, C, st);
   }
-  if (launch_skinny_k<MB, 1, EPI, TR, TC, false>(M, N, K, S, A, W, part, R, C, st)) return -1;
+  if (launch_skinny_k<MB, WN, EPI, TR, TC, false>(M, N, K, S, A, W, part, R, C, st)) return -1;
   return launch_reduce<EPI, TR, TC>(M, N, S, part, R, C, st);
+}
+
+template <int MB, int EPI, typename TR, typename TC>
+static int launch_skinny_mb(int M, int N, int K, SkinnyPlan pl, const void* A, const void* W, float* part,
+                            const void* R, void* C, hipStream_t st) {
+  if (pl.wn == 2) return launch_skinny_wn<MB, 2, EPI, TR, TC>(M, N, K, pl.s, A, W, part, R, C, st);
+  return launch_skinny_wn<MB, 1, EPI, TR, TC>(M, N, K, pl.s, A, W, part, R, C, st);
+}
+
+template <int EPI, typename TR, typename TC>
+static int launch_skinny_plan(int M, int N, int K, SkinnyPlan pl, const void* A, const void* W, float* part,
+                              const void* R, void* C, hipStream_t st) {
+  if ((pl.wn != 1 && pl.wn != 2) || N % (64 * pl.wn) != 0 || pl.s < 1 || K % (skinny::KS * pl.s) != 0) return -1;
+  switch ((M + 15) / 16) {
+    case 1: return launch_skinny_mb<1, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
+    case 2: return launch_skinny_mb<2, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
+    case 3: return launch_skinny_mb<3, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
+    case 4: return launch_skinny_mb<4, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
+    default: return -1;
+  }
 }
 
 template <int EPI, typename TR, typename TC>
 static int launch_skinny(int M, int N, int K, const void* A, const void* W, float* part, const void* R, void* C,
                          hipStream_t st) {
-  const int S = gemm_skinny_splits(M, N, K);
-  switch ((M + 15) / 16) {
-    case 1: return launch_skinny_mb<1, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
-    case 2: return launch_skinny_mb<2, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
-    case 3: return launch_skinny_mb<3, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
-    case 4: return launch_skinny_mb<4, EPI, TR, TC>(M, N, K, S, A, W, part, R, C, st);
-    default: return -1;
-  }
+  return launch_skinny_plan<EPI, TR, TC>(M, N, K, gemm_skinny_plan(M, N, K), A, W, part, R, C, st);
 }
 
 template <int EPI, typename TR, typename TC>
@@ -694,7 +730,7 @@ static int launch_f32(int M, int N, int K, const void* A, const void* W, const v
 
 size_t gemm_workspace_bytes(int dtype, int M, int N, int K) {
   if (dtype != 1 || M > skinny::MAXM) return 0;
-  return (size_t)gemm_skinny_splits(M, N, K) * M * N * sizeof(float);
+  return (size_t)gemm_skinny_plan(M, N, K).s * M * N * sizeof(float);
 }
 
 // Dispatch on (dtype, r_dtype, c_dtype, epilogue) and on M.

@@ -87,6 +87,36 @@ int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, hipStream_t
   return 0;
 }
 
+// Row-major W[N, K] -> 64x64 tiles (layout in common.h): one thread per
+// destination element, zero in the padding of edge tiles. A one-time
+// weight preparation; T is the element's bit pattern (2 or 4 bytes).
+template <typename T>
+__global__ __launch_bounds__(256) void tile_weight_kernel(const T* __restrict__ src, T* __restrict__ dst, long N,
+                                                          long K, long total) {
+  const long kt = (K + kWTile - 1) / kWTile;
+  for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long)gridDim.x * 256) {
+    const long tile = e / kWTileElts, in = e % kWTileElts;
+    const long n = (tile / kt) * kWTile + in / kWTile;
+    const long k = (tile % kt) * kWTile + in % kWTile;
+    dst[e] = (n < N && k < K) ? src[n * K + k] : T(0);
+  }
+}
+
+int launch_tile_weight(int elt_bytes, long N, long K, const void* src, void* dst, hipStream_t st) {
+  const long total = tiled_weight_elems(N, K);
+  if (total == 0) return 0;
+  const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
+  if (elt_bytes == 2)
+    hipLaunchKernelGGL(tile_weight_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, (const uint16_t*)src,
+                       (uint16_t*)dst, N, K, total);
+  else if (elt_bytes == 4)
+    hipLaunchKernelGGL(tile_weight_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st, (const uint32_t*)src,
+                       (uint32_t*)dst, N, K, total);
+  else
+    return -1;
+  return 0;
+}
+
 int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st) {
   if (rows == 0) return 0;
   if (d % 8) return -1;

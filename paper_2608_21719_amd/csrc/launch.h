@@ -36,7 +36,11 @@ int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* p
 int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
                 const void* R, void* C, void* ws, size_t ws_bytes, hipStream_t st);
 size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
-int gemm_skinny_splits(int M, int N, int K);
+struct SkinnyPlan {
+  int wn;  // 64-row weight blocks per workgroup (1 or 2)
+  int s;   // K splits
+};
+SkinnyPlan gemm_skinny_plan(int M, int N, int K);
 int gemm_check(int dtype, int epi, int M, int N, int K);
 
 // model-level kernels (bf16 rows)
@@ -44,5 +48,6 @@ int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, hipStream_t
 int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st);
 int launch_gather_rows(int n, int d, const void* src, const int32_t* rows, void* dst, hipStream_t st);
 int launch_argmax(int rows, int vocab, const float* logits, int32_t* next, hipStream_t st);
+int launch_tile_weight(int elt_bytes, long N, long K, const void* src, void* dst, hipStream_t st);
 
 }  // namespace ps

@@ -30,6 +30,13 @@ def to_dev(a, dtype: str):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
 
 
+def to_dev_w(w, dtype: str):
+    """Row-major [N, K] linear weight (storage array) -> device tensor in the
+    library's tiled weight layout (tiling by the library's host helper)."""
+    from paper_2608_21719_amd import binding as B
+    return to_dev(B.tile_weight(np.ascontiguousarray(w)), dtype)
+
+
 def to_f64(t) -> np.ndarray:
     """Device tensor (bf16 or fp32) -> float64 numpy, exactly."""
     torch = torch_mod()
@@ -90,11 +97,11 @@ class DeviceLayer:
         self.dtype = dtype
         self.t = {
             "attn_norm": to_dev(w["attn_norm"], dtype),
-            "w_qkv": to_dev(np.concatenate([w["wq"], w["wk"], w["wv"]], axis=0), dtype),
-            "w_o": to_dev(w["wo"], dtype),
+            "w_qkv": to_dev_w(np.concatenate([w["wq"], w["wk"], w["wv"]], axis=0), dtype),
+            "w_o": to_dev_w(w["wo"], dtype),
             "ffn_norm": to_dev(w["ffn_norm"], dtype),
-            "w_gate_up": to_dev(B.pack_gate_up(w["wg"], w["wu"]), dtype),
-            "w_down": to_dev(w["wd"], dtype),
+            "w_gate_up": to_dev_w(B.pack_gate_up(w["wg"], w["wu"]), dtype),
+            "w_down": to_dev_w(w["wd"], dtype),
         }
         self.w = B.layer_weights(**self.t)
 

@@ -163,6 +163,33 @@ def test_pack_gate_up_layout():
     np.testing.assert_array_equal(out[96:128], wu[32:64])
 
 
+@pytest.mark.parametrize("N,K,dt", [(128, 192, np.uint16), (100, 70, np.uint16), (65, 129, np.float32),
+                                    (1, 1, np.float32), (64, 64, np.uint16)])
+def test_tile_weight_layout(N, K, dt):
+    """The tiled weight layout: pad W to multiples of 64 with zeros, cut it
+    into 64 x 64 tiles, order the tiles row of tiles by row of tiles, each
+    tile row-major; also the per-element address formula of the header."""
+    r = np.random.default_rng(N * 1000 + K)
+    w = r.integers(1, 1 << 15, size=(N, K)).astype(dt)  # nonzero, so padding is visible
+    out = B.tile_weight(w)
+    nt, kt = -(-N // 64), -(-K // 64)
+    assert out.shape == (nt * kt * 4096,) == (B.tiled_weight_elems(N, K),)
+    pad = np.zeros((nt * 64, kt * 64), dtype=dt)
+    pad[:N, :K] = w
+    want = pad.reshape(nt, 64, kt, 64).transpose(0, 2, 1, 3).reshape(-1)
+    np.testing.assert_array_equal(out, want)
+    n, k = r.integers(0, N, 50), r.integers(0, K, 50)
+    np.testing.assert_array_equal(out[((n // 64) * kt + k // 64) * 4096 + (n % 64) * 64 + k % 64], w[n, k])
+
+
+def test_tile_weight_rejects_bad_arguments():
+    assert B.tiled_weight_elems(0, 5) == 0 and B.tiled_weight_elems(5, -1) == 0
+    w = np.zeros((4, 4), np.uint8)
+    out = np.zeros(4096, np.uint8)
+    assert B.lib.ps_tile_weight(B.ptr(w), 4, 4, 1, B.ptr(out)) == B.PS_E_INVALID
+    assert B.lib.ps_tile_weight(None, 4, 4, 2, B.ptr(out)) == B.PS_E_INVALID
+
+
 def test_workspace_and_pool_sizes():
     sh = CONFIGS["llama8b_decode"].shape
     cfg = B.make_cfg(sh)

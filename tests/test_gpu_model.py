@@ -56,9 +56,11 @@ def test_lm_head_gemm_fullsize_sampled_columns():
     g = torch.Generator(device="cuda").manual_seed(5)
     a = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
     w = (torch.randn((N, K), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    wt = torch.empty(B.tiled_weight_elems(N, K), dtype=torch.bfloat16, device="cuda")
+    B.op_tile_weight(B.PS_BF16, N, K, w, wt)
     c = torch.empty((M, N), dtype=torch.float32, device="cuda")
     ws = H.workspace(B.op_gemm_workspace_bytes(B.PS_BF16, M, N, K))
-    B.op_gemm(B.PS_BF16, 0, B.PS_F32, B.PS_EPI_STORE, M, N, K, a, w, None, c, ws)
+    B.op_gemm(B.PS_BF16, 0, B.PS_F32, B.PS_EPI_STORE, M, N, K, a, wt, None, c, ws)
     sync()
     cols = np.sort(np.random.default_rng(2).choice(N, 300, replace=False))
     af = H.to_f64(a)
@@ -99,7 +101,7 @@ def test_small_model_prefill_then_decode():
     layers_f = [H.weights_f64(w, "bf16") for w in layers]
     head_f = H.weights_f64(head, "bf16")
     dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
-    dev_head = {k: H.to_dev(v, "bf16") for k, v in head.items()}
+    dev_head = {k: (H.to_dev_w if k == "lm_head" else H.to_dev)(v, "bf16") for k, v in head.items()}
     pool = H.Pool(sh, 64, 4, 8, n_layers=L, seed=21)
     model = B.Model(pool.cfg, [d.w for d in dev_layers], V, dev_head["embed"], dev_head["final_norm"],
                     dev_head["lm_head"])
@@ -147,7 +149,7 @@ def test_small_model_prefill_then_decode():
 def test_model_rejects_shallow_pool():
     wl, layers, head = small_model_parts(n_layers=2, vocab=256)
     dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
-    dev_head = {k: H.to_dev(v, "bf16") for k, v in head.items()}
+    dev_head = {k: (H.to_dev_w if k == "lm_head" else H.to_dev)(v, "bf16") for k, v in head.items()}
     pool = H.Pool(wl.shape, 8, 2, 4, n_layers=1)
     model = B.Model(pool.cfg, [d.w for d in dev_layers], 256, dev_head["embed"], dev_head["final_norm"],
                     dev_head["lm_head"])

@@ -63,11 +63,12 @@ def gemm_bound(a, w, K, out_bf16):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 512, 448), (256, 256, 64), (520, 768, 1024),   # tile path
-                                   (64, 256, 1024), (37, 192, 512), (1, 64, 256), (17, 320, 2048)])  # skinny
+                                   (64, 256, 1024), (37, 192, 512), (1, 64, 256), (17, 320, 2048),  # skinny
+                                   (64, 32768, 256), (33, 16384, 2048)])  # skinny, two blocks per workgroup
 def test_gemm_store_bf16(M, N, K):
     a = rnd((M, K), "bf16", 3)
     w = rnd((N, K), "bf16", 4, 0.02)
-    A, W = H.to_dev(a, "bf16"), H.to_dev(w, "bf16")
+    A, W = H.to_dev(a, "bf16"), H.to_dev_w(w, "bf16")
     C = H.empty((M, N), "bf16")
     ws = H.workspace(B.op_gemm_workspace_bytes(B.PS_BF16, M, N, K))
     B.op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_STORE, M, N, K, A, W, None, C, ws)
@@ -79,13 +80,14 @@ def test_gemm_store_bf16(M, N, K):
     assert np.all(err <= absb + relb * np.abs(ref)), f"max err {err.max()}"
 
 
-@pytest.mark.parametrize("M,N,K", [(300, 512, 448), (64, 256, 1024), (5, 128, 256)])
+@pytest.mark.parametrize("M,N,K", [(300, 512, 448), (64, 256, 1024), (5, 128, 256), (64, 256, 4096), (64, 16384, 2048),
+                                   (40, 20480, 128)])
 @pytest.mark.parametrize("rdt,cdt", [("bf16", "f32"), ("f32", "bf16")])
 def test_gemm_residual(M, N, K, rdt, cdt):
     a = rnd((M, K), "bf16", 5)
     w = rnd((N, K), "bf16", 6, 0.02)
     r = rnd((M, N), rdt, 7)
-    A, W, R = H.to_dev(a, "bf16"), H.to_dev(w, "bf16"), H.to_dev(r, rdt)
+    A, W, R = H.to_dev(a, "bf16"), H.to_dev_w(w, "bf16"), H.to_dev(r, rdt)
     C = H.empty((M, N), cdt)
     ws = H.workspace(B.op_gemm_workspace_bytes(B.PS_BF16, M, N, K))
     code = {"f32": B.PS_F32, "bf16": B.PS_BF16}
@@ -98,13 +100,14 @@ def test_gemm_residual(M, N, K, rdt, cdt):
     assert np.all(err <= absb + relb * np.abs(ref) + 1e-7 * np.abs(ref)), f"max err {err.max()}"
 
 
-@pytest.mark.parametrize("M,F,K", [(300, 256, 448), (64, 192, 1024), (3, 64, 256)])
+@pytest.mark.parametrize("M,F,K", [(300, 256, 448), (64, 192, 1024), (3, 64, 256), (64, 16384, 256), (20, 8192, 1024),
+                                   (20, 8192, 2048), (20, 384, 2048)])
 def test_gemm_swiglu(M, F, K):
     a = rnd((M, K), "bf16", 8)
     wg = rnd((F, K), "bf16", 9, 0.05)
     wu = rnd((F, K), "bf16", 10, 0.05)
     A = H.to_dev(a, "bf16")
-    W = H.to_dev(B.pack_gate_up(wg, wu), "bf16")
+    W = H.to_dev_w(B.pack_gate_up(wg, wu), "bf16")
     C = H.empty((M, F), "bf16")
     ws = H.workspace(B.op_gemm_workspace_bytes(B.PS_BF16, M, 2 * F, K))
     B.op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_SWIGLU, M, 2 * F, K, A, W, None, C, ws)
@@ -114,15 +117,14 @@ def test_gemm_swiglu(M, F, K):
     H.assert_close_elementwise(H.to_f64(C), ref, 1e-3, 2 ** -7, "swiglu")
 
 
-@pytest.mark.parametrize("epi", [0, 1, 2])
+@pytest.mark.parametrize("epi,N,K", [(0, 128, 256), (1, 128, 256), (2, 128, 256), (0, 100, 70), (1, 70, 130)])
 @pytest.mark.parametrize("M", [512, 4, 70])
-def test_gemm_f32(epi, M):
-    N, K = 128, 256
+def test_gemm_f32(epi, N, K, M):
     a = rnd((M, K), "f32", 11)
     w = rnd((N, K), "f32", 12, 0.05)
     r = rnd((M, N), "f32", 13)
     wdev = B.pack_gate_up(w[:N // 2], w[N // 2:]) if epi == 2 else w
-    A, W, R = H.to_dev(a, "f32"), H.to_dev(wdev, "f32"), H.to_dev(r, "f32")
+    A, W, R = H.to_dev(a, "f32"), H.to_dev_w(wdev, "f32"), H.to_dev(r, "f32")
     C = H.empty((M, N // 2 if epi == 2 else N), "f32")
     B.op_gemm(B.PS_F32, B.PS_F32, B.PS_F32, epi, M, N, K, A, W, R if epi == 1 else None, C)
     sync()
@@ -132,6 +134,18 @@ def test_gemm_f32(epi, M):
     else:
         ref = O.linear(af, wf) + (r if epi == 1 else 0)
     H.assert_close_elementwise(H.to_f64(C), ref, 1e-5, 1e-5, "gemm f32")
+
+
+@pytest.mark.parametrize("dt,N,K", [("bf16", 192, 320), ("bf16", 100, 70), ("f32", 65, 129), ("f32", 1, 1)])
+def test_op_tile_weight_matches_host_tiling(dt, N, K):
+    """Device tiling is bit-identical to the host helper, padding included."""
+    w = rnd((N, K), dt, 14)
+    code = B.PS_BF16 if dt == "bf16" else B.PS_F32
+    out = H.empty((B.tiled_weight_elems(N, K),), dt)
+    out.fill_(1.0)  # padding must be written, not left over
+    B.op_tile_weight(code, N, K, H.to_dev(w, dt), out)
+    sync()
+    np.testing.assert_array_equal(H.bits(out), H.bits(H.to_dev_w(w, dt)))
 
 
 def test_gemm_rejects_unsupported_shape():
