@@ -5,10 +5,10 @@
 // workgroup streams is then one contiguous 8 KiB (bf16) block of HBM rather
 // than 64 strided 128-byte pieces. fp32 accumulation (gfx950).
 //
-//  * gemm_tile_kernel: prefill-sized M. 256x256x64 workgroup tile, eight
-//    waves of 128x64 (two per SIMD), v_mfma_f32_16x16x32_bf16, operands
-//    staged through double-buffered, XOR-swizzled LDS (128 KiB) by direct
-//    global->LDS loads. MFMA-bound.
+//  * gemm_tile_kernel: prefill-sized M. 256x256 workgroup tile, four waves
+//    of 128x128 (one per SIMD), v_mfma_f32_32x32x16_bf16 with accumulators
+//    in AGPRs, 64-k stages in two XOR-swizzled LDS slots (128 KiB) filled
+//    by direct global->LDS loads spread over the stage. MFMA-bound.
 //  * gemm_skinny_kernel: decode-sized M (<= 64). Streams W once from HBM
 //    with 16-byte loads, one 16-column MFMA block per wave, activations
 //    staged in LDS and shared by the workgroup's four waves; K may be split
@@ -26,6 +26,14 @@
 namespace ps {
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
+// silu on the hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32): a few
+// fp32 ulp, far below the bf16 rounding of the GEMM operands; four vector
+// instructions instead of the ~30 of expf and an IEEE divide, which matter
+// in an epilogue that no matrix work overlaps. x -> -inf gives -0, x -> inf
+// gives x.
+__device__ __forceinline__ float silu_fast(float x) {
+  return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x * -1.4426950408889634f));
+}
 
 template <typename T> __device__ __forceinline__ float ld_elt(const T* p, long i);
 template <> __device__ __forceinline__ float ld_elt<float>(const float* p, long i) { return p[i]; }
@@ -34,40 +42,11 @@ template <typename T> __device__ __forceinline__ void st_elt(T* p, long i, float
 template <> __device__ __forceinline__ void st_elt<float>(float* p, long i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st_elt<bf16_t>(bf16_t* p, long i, float v) { p[i] = f2bf(v); }
 
-// ====================================================================== tile
-// Workgroup tile BM x BN, K step BK, WAVES_M x WAVES_N waves, STAGES-deep
-// ring of LDS buffers filled by direct global->LDS loads
-// (global_load_lds_dwordx4): one wave instruction fills 1 KiB of LDS, lane l
-// landing at +16 l. LDS rows hold BK bf16 (BK/8 16-byte chunks), XOR-
-// swizzled so that the 16-byte operand reads of 16 consecutive rows hit 16
-// distinct 16-byte bank groups; the global address of each lane is chosen
-// so that the linear fill lands in swizzled order.
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_>
-struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
-  static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
-  static constexpr int NW = WAVES_M * WAVES_N;
-  static constexpr int NT = 64 * NW;
-  static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
-  static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 MFMA blocks per wave
-  static constexpr int CPR = BK / 8;               // 16-byte chunks per LDS row
-  static constexpr int ROWS_PER_LOAD = 64 / CPR;   // rows one wave instruction fills
-  static constexpr int A_ELTS = BM * BK, B_ELTS = BN * BK;
-  static constexpr int STAGE_ELTS = A_ELTS + B_ELTS;
-  static constexpr int A_LOADS = BM / ROWS_PER_LOAD / NW;  // per wave per stage
-  static constexpr int B_LOADS = BN / ROWS_PER_LOAD / NW;
-  static constexpr int LOADS = A_LOADS + B_LOADS;
-  static constexpr size_t LDS_BYTES = (size_t)STAGES * STAGE_ELTS * 2;
-  static_assert(FM >= 1 && FN >= 1 && A_LOADS >= 1 && B_LOADS >= 1, "tile shape");
-  static_assert(BM % (ROWS_PER_LOAD * NW) == 0 && BN % (ROWS_PER_LOAD * NW) == 0, "load split");
-  __device__ static int swz(int row, int ch) {
-    return row * BK + ((ch ^ ((row / (16 / CPR)) % CPR)) << 3);
-  }
-};
-
-// One 16-byte global->LDS fill per lane (global_load_lds_dwordx4). Kept in
-// a non-template device function: used directly inside a kernel template
-// the builtin makes the host pass drop the kernel's instantiation.
+// ================================================================== helpers
+// One 16-byte global->LDS fill per lane (global_load_lds_dwordx4): a wave
+// instruction fills 1 KiB of LDS, lane l landing at +16 l. Kept in a
+// non-template device function: used directly inside a kernel template the
+// builtin makes the host pass drop the kernel's instantiation.
 __device__ __forceinline__ void load_lds16(const bf16_t* g, bf16_t* lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
@@ -86,270 +65,295 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 // memory clobber keeps LDS accesses on their side of the barrier.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// bf16 store and SwiGLU epilogues stage the output tile in LDS
-template <int EPI, typename TC>
-constexpr bool staged_epilogue() { return EPI != 1 && std::is_same<TC, bf16_t>::value; }
-template <class CF, int EPI>
-constexpr int tile_out_stride() { return (EPI == 2 ? CF::BN / 2 : CF::BN) * 2 + 16; }
-template <class CF>
-constexpr int tile_res_stride() { return CF::BN * 4 + 16; }
-template <class CF, int EPI, typename TC>
-constexpr size_t tile_lds_bytes() {
-  const size_t staged = staged_epilogue<EPI, TC>() ? (size_t)CF::BM * tile_out_stride<CF, EPI>()
-                        : EPI == 1                ? (size_t)(CF::BM / 2) * tile_res_stride<CF>()
-                                                  : 0;
-  return CF::LDS_BYTES > staged ? CF::LDS_BYTES : staged;
+// The same barrier pinned in the instruction schedule: register-only work
+// (MFMAs) may not move across it either.
+__device__ __forceinline__ void lds_barrier_pinned() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
-template <class CF, int EPI, typename TR, typename TC>
-__global__ __launch_bounds__(CF::NT) void gemm_tile_kernel(
-    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, const TR* __restrict__ R, TC* __restrict__ C,
-    int M, int N, int K, int tiles_n) {
-  constexpr int BM = CF::BM, BN = CF::BN, BK = CF::BK, STAGES = CF::STAGES;
+// ====================================================================== tile
+// Prefill-sized M. Workgroup tile 256 x 256, four waves of 128 x 128 (one
+// per SIMD), v_mfma_f32_32x32x16_bf16 with the 256 accumulators per lane in
+// AGPRs. K runs in 64-wide stages through two LDS slots (128 KiB) filled by
+// global->LDS DMA; LDS rows are 128 B, their 16-byte chunks XOR-swizzled by
+// (row / 2) % 8 so that the operand reads of 16 consecutive rows hit 16
+// distinct bank groups (the DMA lane addresses are chosen so that the
+// linear fill lands swizzled).
+//
+// Schedule of stage st (slot st & 1), four 16-k slices of 16 MFMAs each:
+//  * slices 0..2: after two MFMAs, read the next slice's fragments in one
+//    burst (the compiler waits for every outstanding LDS read before the
+//    first MFMA that uses a fragment, so a burst issued early has ~14 MFMAs
+//    to land); slices 0 and 1 also issue the second part of the DMA of
+//    stage st+1;
+//  * wait for stage st+1 and this stage's reads, one barrier;
+//  * slice 3: read stage st+1's first fragments, and issue the first part
+//    of stage st+2's DMA into slot st & 1, whose last reads are complete.
+// Spreading a stage's 16 DMA instructions per wave over three slices keeps
+// the address unit from backing up: issued as one burst they stall the
+// waves' instruction streams (the cost was per instruction, not per byte).
+namespace tile {
+constexpr int BM = 256, BN = 256, BK = 64, NT = 256, WT = 128;
+constexpr int CPR = BK / 8, RPL = 64 / CPR;                         // 8 chunks per row, 8 rows per DMA
+constexpr int A_ELTS = BM * BK, STAGE = (BM + BN) * BK;             // bf16 elements
+constexpr int A_LOADS = BM / RPL / 4, B_LOADS = BN / RPL / 4, LOADS = A_LOADS + B_LOADS;  // per wave
+constexpr int Q = WT / 32;                                           // 4 x 4 blocks of 32 x 32
+constexpr int D3 = 6, D0 = 5, D1 = LOADS - D3 - D0;                  // DMA split over slices 3, 0, 1
+constexpr size_t LDS_BYTES = 2 * (size_t)STAGE * 2;
+__device__ __forceinline__ int swz(int row, int ch) { return row * BK + ((ch ^ ((row >> 1) & 7)) << 3); }
+}  // namespace tile
+
+template <int EPI, typename TR, typename TC>
+__global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+                                                        const TR* __restrict__ R, TC* __restrict__ C, int M, int N,
+                                                        int K, int tiles_n, int group) {
+  using namespace tile;
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
 
   // XCD-aware tile order: consecutive workgroup ids go round-robin over the
-  // 8 XCDs; give each XCD a contiguous range of tiles so that tiles sharing
-  // A rows and W rows meet in the same L2.
+  // 8 XCDs; give each XCD a contiguous range of tiles, walked in groups of
+  // `group` tile-rows across N, so that tiles sharing A and W panels meet in
+  // the same L2.
   const int nwg = gridDim.x;
   int id = blockIdx.x;
   if ((nwg & 7) == 0) id = (id & 7) * (nwg >> 3) + (id >> 3);
-  // within that order, walk groups of 4 tile-rows across N
-  constexpr int GROUP = 4;
   const int tiles_m = nwg / tiles_n;
-  const int group_sz = GROUP * tiles_n;
-  const int grp = id / group_sz;
-  const int first_m = grp * GROUP;
-  const int gm = min(GROUP, tiles_m - first_m);
+  const int group_sz = group * tiles_n;
+  const int first_m = (id / group_sz) * group;
+  const int gm = min(group, tiles_m - first_m);
   const int tm = first_m + (id % group_sz) % gm;
   const int tn = (id % group_sz) / gm;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const int wm = wave / CF::WAVES_N, wn = wave % CF::WAVES_N;
-  const int g = lane >> 4, c = lane & 15;  // 16x16x32 operand / result lane roles
-
-  // per-lane global sources of this wave's loads (row block of the wave)
-  const int lrow = lane / CF::CPR, lpos = lane % CF::CPR;
-  const bf16_t* ga[CF::A_LOADS];
-  const bf16_t* gb[CF::B_LOADS];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  // DMA sources: a workgroup-uniform base plus a 32-bit lane offset (elements)
+  const int lrow = lane / CPR, lpos = lane % CPR;
+  uint32_t aoff[A_LOADS], boff[B_LOADS];
 #pragma unroll
-  for (int i = 0; i < CF::A_LOADS; ++i) {
-    const int row = (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD + lrow;
-    const int ch = lpos ^ ((row / (16 / CF::CPR)) % CF::CPR);
-    ga[i] = A + (long)min(m0 + row, M - 1) * K + ch * 8;
+  for (int i = 0; i < A_LOADS; ++i) {
+    const int row = (wave * A_LOADS + i) * RPL + lrow;
+    aoff[i] = (uint32_t)(min(m0 + row, M - 1) - m0) * K + (lpos ^ ((row >> 1) & 7)) * 8;
   }
 #pragma unroll
-  for (int i = 0; i < CF::B_LOADS; ++i) {
-    const int row = (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD + lrow;
-    const int ch = lpos ^ ((row / (16 / CF::CPR)) % CF::CPR);
-    const int n = n0 + row;  // tiled W: k-tile kt of row n at ((n/64) K/64 + kt) 4096 + (n%64) 64
-    gb[i] = W + (long)(n >> 6) * (K / 64) * kWTileElts + (n & 63) * 64 + ch * 8;
+  for (int i = 0; i < B_LOADS; ++i) {  // tiled W: rows of 64-row block row/64, k-tile added per stage
+    const int row = (wave * B_LOADS + i) * RPL + lrow;
+    boff[i] = (uint32_t)(row >> 6) * (K / 64) * kWTileElts + (row & 63) * 64 + (lpos ^ ((row >> 1) & 7)) * 8;
   }
-  static_assert(BK == 64, "one W tile per k step");
-  auto gload = [&](int kt, int stage) {
-    bf16_t* a = smem + stage * CF::STAGE_ELTS;
-    bf16_t* b = a + CF::A_ELTS;
-#pragma unroll
-    for (int i = 0; i < CF::A_LOADS; ++i)
-      load_lds16(ga[i] + kt * BK, a + (wave * CF::A_LOADS + i) * CF::ROWS_PER_LOAD * BK);
-#pragma unroll
-    for (int i = 0; i < CF::B_LOADS; ++i)
-      load_lds16(gb[i] + (long)kt * kWTileElts, b + (wave * CF::B_LOADS + i) * CF::ROWS_PER_LOAD * BK);
+  const bf16_t* Ablk = A + (long)m0 * K;
+  const bf16_t* Wblk = W + (long)(n0 >> 6) * (K / 64) * kWTileElts;
+  static_assert(BK == kWTile, "one W tile per stage");
+  // DMA instruction l (0..LOADS-1) of stage s into slot s & 1
+  auto dma = [&](int s, int l) {
+    bf16_t* st = smem + (s & 1) * STAGE;
+    if (l < A_LOADS)
+      load_lds16(Ablk + s * BK + aoff[l], st + (wave * A_LOADS + l) * RPL * BK);
+    else
+      load_lds16(Wblk + (long)s * kWTileElts + boff[l - A_LOADS], st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
   };
 
-  // operand fragments, double-buffered in registers across 32-wide k steps:
-  // lane (g, c) holds row c of a 16-row block, k = 8 g .. 8 g + 7 of the step
-  constexpr int FM = CF::FM, FN = CF::FN, KK = BK / 32;
-  static_assert(KK % 2 == 0, "register double-buffering alternates buffers by k-step parity");
-  bf16x8_t fa[2][FM], fb[2][FN];
-  auto frags = [&](int slot, int kk, int p) {
-    const bf16_t* a = smem + slot * CF::STAGE_ELTS;
-    const bf16_t* b = a + CF::A_ELTS;
+  // 32x32x16 operands: lane (h, r) holds row r of a 32-row block, k 8h..8h+7
+  // of a 16-k slice; fragments double-buffered by slice parity
+  const int h = lane >> 5, r32 = lane & 31;
+  bf16x8_t fa[2][Q], fb[2][Q];
+  auto read_frags = [&](int slot, int sl) {
+    const bf16_t* a = smem + slot * STAGE;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-      fa[p][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + CF::swz(wm * CF::WTM + i * 16 + c, 4 * kk + g)));
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-      fb[p][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(b + CF::swz(wn * CF::WTN + j * 16 + c, 4 * kk + g)));
-  };
-  f32x4_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  auto mfmas = [&](int p) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
-  };
-  // issue order for one k step: the next step's LDS reads spread evenly
-  // between this step's MFMAs, so read latency hides under matrix work
-  auto interleave = [&]() {
-    constexpr int RATIO = (FM * FN) / (FM + FN) > 0 ? (FM * FN) / (FM + FN) : 1;
-#pragma unroll
-    for (int q = 0; q < FM + FN; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, RATIO, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // LDS read
+    for (int i = 0; i < Q; ++i) {
+      fa[sl & 1][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + swz(wm * WT + i * 32 + r32, 2 * sl + h)));
+      fb[sl & 1][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + A_ELTS + swz(wn * WT + i * 32 + r32, 2 * sl + h)));
     }
-    if constexpr (FM * FN > RATIO * (FM + FN))
-      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - RATIO * (FM + FN), 0);
+  };
+  f32x16_t acc[Q][Q];
+#pragma unroll
+  for (int i = 0; i < Q; ++i)
+#pragma unroll
+    for (int j = 0; j < Q; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // an (empty) AGPR operand makes the compiler select the AGPR form of the
+  // MFMAs, which keeps the accumulators in place in the AGPR file
+  asm volatile("" ::"a"(0.f));
+  auto mfma = [&](int sl, int q) {
+    acc[q / Q][q % Q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[sl & 1][q / Q], fb[sl & 1][q % Q], acc[q / Q][q % Q], 0, 0, 0);
   };
 
-  const int KT = K / BK;
-  // prologue: stages 0 .. STAGES-2 in flight; stage 0 landed everywhere;
-  // stage STAGES-1 issued; fragments of (stage 0, k step 0) requested
+  const int T = K / BK;
+  // stage st; `full` = st + 2 < T (every condition below holds)
+  auto stage = [&](int st, bool full) {
+    const int slot = st & 1;
+    const bool more = full || st + 1 < T;
+    const bool dma_next = st > 0 && st + 1 < T;  // rest of stage st+1 (stage 1 comes whole with the prologue)
+    auto slice = [&](auto slc) {
+      constexpr int sl = decltype(slc)::value;
+      constexpr int DN = sl == 0 ? D0 : sl == 1 ? D1 : 0;
+      constexpr int DB = D3 + (sl == 1 ? D0 : 0);
+      mfma(sl, 0);
+      mfma(sl, 1);
+      read_frags(slot, sl + 1);
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < KT) gload(st, st);
-  if (STAGES - 2 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
-  else wait_vmcnt_lgkm0<0>();
-  lds_barrier();
-  if (STAGES - 1 < KT) gload(STAGES - 1, STAGES - 1);
-  frags(0, 0, 0);
-  for (int kt = 0; kt < KT; ++kt) {
-    const int slot = kt % STAGES;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int p = kk & 1;
-      if (kk < KK - 1) {
-        frags(slot, kk + 1, p ^ 1);
-        mfmas(p);
-        interleave();
-      } else {
-        mfmas(p);
-        if (kt + 1 < KT) {
-          // stage kt+1 has landed for this wave and this wave's reads of
-          // stage kt have returned; after the barrier both hold for all
-          // waves, so slot kt may be refilled with stage kt+STAGES
-          if (kt + STAGES - 1 < KT) wait_vmcnt_lgkm0<(STAGES - 2) * CF::LOADS>();
-          else wait_vmcnt_lgkm0<0>();
-          lds_barrier();
-          if (kt + STAGES < KT) gload(kt + STAGES, slot);
-          frags((kt + 1) % STAGES, 0, p ^ 1);
-        }
+      for (int q = 2; q < Q * Q; ++q) {
+        mfma(sl, q);
+        if (DN > 0 && q - 2 < DN && dma_next) dma(st + 1, DB + q - 2);
       }
+      if (full) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);       // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * Q, 0);   // LDS read
+#pragma unroll
+        for (int k = 0; k < DN; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);     // VMEM read (DMA)
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, Q * Q - 2 - DN, 0);
+      }
+    };
+    slice(std::integral_constant<int, 0>{});
+    slice(std::integral_constant<int, 1>{});
+    slice(std::integral_constant<int, 2>{});
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) {
+      wait_vmcnt_lgkm0<0>();  // stage st+1 landed, this stage's reads returned
+      lds_barrier_pinned();
     }
-  }
+    mfma(3, 0);
+    mfma(3, 1);
+    if (more) read_frags(slot ^ 1, 0);
+#pragma unroll
+    for (int q = 2; q < Q * Q; ++q) {
+      mfma(3, q);
+      if (q - 2 < D3 && full) dma(st + 2, q - 2);
+    }
+    if (full) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * Q, 0);
+#pragma unroll
+      for (int k = 0; k < D3; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, Q * Q - 2 - D3, 0);
+    }
+  };
 
-  // epilogue: acc[i][j][r] = C[row 16 i + 4 g + r][col 16 j + c] of the wave tile.
-  // SwiGLU pairs: the wave's columns hold 32-row gate/up blocks alternately,
-  // so gate n-block jg = 4 (jp / 2) + jp % 2 pairs with up n-block jg + 2.
-  const int rbase = m0 + wm * CF::WTM, cbase = n0 + wn * CF::WTN;
-  auto gate_nb = [](int jp) { return 4 * (jp >> 1) + (jp & 1); };
-  auto gate_col = [](int jp) { return 32 * (jp >> 1) + 16 * (jp & 1); };  // wave-local output column
-  if constexpr (staged_epilogue<EPI, TC>()) {
-    // bf16 results go through LDS (free after the main loop) so that global
-    // stores are whole 16-byte chunks of full rows rather than 2-byte
-    // scatters; padded rows put the four lane groups (rows 4 apart) on
-    // different banks
-    constexpr int OCOLS = EPI == 2 ? BN / 2 : BN;
-    constexpr int OSTRIDE = tile_out_stride<CF, EPI>();  // bytes per staged row
-    char* so = (char*)smem;
-    __syncthreads();  // every wave is done reading operand tiles
+  // prologue: stages 0 and 1 whole, stage 0 landed everywhere, its first
+  // fragments read
 #pragma unroll
-    for (int i = 0; i < CF::FM; ++i)
+  for (int l = 0; l < LOADS; ++l) dma(0, l);
+  if (T > 1) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int lrow = wm * CF::WTM + i * 16 + 4 * g + r;
-        if constexpr (EPI == 2) {
-#pragma unroll
-          for (int jp = 0; jp < CF::FN / 2; ++jp) {
-            const int lcol = (wn * CF::WTN >> 1) + gate_col(jp) + c;
-            const int jg = gate_nb(jp);
-            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(silu_f(acc[i][jg][r]) * acc[i][jg + 2][r]);
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < CF::FN; ++j) {
-            const int lcol = wn * CF::WTN + j * 16 + c;
-            *(bf16_t*)(so + lrow * OSTRIDE + lcol * 2) = f2bf(acc[i][j][r]);
-          }
-        }
-      }
-    __syncthreads();
-    constexpr int CHUNKS = OCOLS / 8;  // 16-byte chunks per row
-    const long ldc = EPI == 2 ? N / 2 : N;
-    const int ocol0 = EPI == 2 ? n0 / 2 : n0;
-    for (int q = t; q < BM * CHUNKS; q += CF::NT) {
-      const int lrow = q / CHUNKS, ch = q - lrow * CHUNKS;
-      if (m0 + lrow < M)
-        *(uint4*)(C + (long)(m0 + lrow) * ldc + ocol0 + ch * 8) = *(const uint4*)(so + lrow * OSTRIDE + ch * 16);
-    }
-  } else if constexpr (EPI == 1) {
-    // residual: the fp32 tile goes through LDS in two halves of 128 rows
-    // (the waves with wm == half write theirs), then every thread adds R and
-    // stores 4 consecutive columns per access; rows of 1040 B put the four
-    // lane groups (rows 4 apart) on different banks
-    static_assert(CF::WAVES_M == 2 && CF::WTM * 2 == BM, "two row halves of the tile");
-    constexpr int HROWS = BM / 2;
-    constexpr int FSTRIDE = tile_res_stride<CF>();  // bytes per staged row
-    char* so = (char*)smem;
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      __syncthreads();  // operand tiles (first half) or the previous half are no longer read
-      if (wm == half) {
-#pragma unroll
-        for (int i = 0; i < CF::FM; ++i)
-#pragma unroll
-          for (int j = 0; j < CF::FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int lrow = i * 16 + 4 * g + r;
-              const int lcol = wn * CF::WTN + j * 16 + c;
-              *(float*)(so + lrow * FSTRIDE + lcol * 4) = acc[i][j][r];
-            }
-      }
-      __syncthreads();
-      constexpr int CHUNKS = BN / 4;  // 4 columns per access
-      for (int q = t; q < HROWS * CHUNKS; q += CF::NT) {
-        const int lrow = q / CHUNKS, ch = q - lrow * CHUNKS;
-        const int row = m0 + half * HROWS + lrow;
-        if (row >= M) continue;
-        const float4 v = *(const float4*)(so + lrow * FSTRIDE + ch * 16);
-        const long idx = (long)row * N + n0 + ch * 4;
-        float o[4] = {v.x, v.y, v.z, v.w};
-        if constexpr (std::is_same<TR, float>::value) {
-          const float4 rr = *(const float4*)(R + idx);
-          o[0] += rr.x; o[1] += rr.y; o[2] += rr.z; o[3] += rr.w;
-        } else {
-          const uint2 rr = *(const uint2*)(R + idx);
-          o[0] += bf_lo(rr.x); o[1] += bf_hi(rr.x); o[2] += bf_lo(rr.y); o[3] += bf_hi(rr.y);
-        }
-        if constexpr (std::is_same<TC, float>::value) {
-          *(float4*)(C + idx) = make_float4(o[0], o[1], o[2], o[3]);
-        } else {
-          *(uint2*)(C + idx) = make_uint2(pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3]));
-        }
-      }
-    }
-  } else if constexpr (EPI == 2) {
-    const int ldc = N / 2;
-#pragma unroll
-    for (int i = 0; i < CF::FM; ++i)
-#pragma unroll
-      for (int jp = 0; jp < CF::FN / 2; ++jp)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = rbase + i * 16 + 4 * g + r;
-          if (row < M) {
-            const int jg = gate_nb(jp);
-            const int col = (cbase >> 1) + gate_col(jp) + c;
-            st_elt<TC>(C, (long)row * ldc + col, silu_f(acc[i][jg][r]) * acc[i][jg + 2][r]);
-          }
-        }
+    for (int l = 0; l < LOADS; ++l) dma(1, l);
+    wait_vmcnt_lgkm0<LOADS>();
   } else {
+    wait_vmcnt_lgkm0<0>();
+  }
+  lds_barrier_pinned();
+  read_frags(0, 0);
+  int st = 0;
+  for (; st + 2 < T; ++st) stage(st, true);
+  for (; st < T; ++st) stage(st, false);
+
+  // epilogue: acc[i][j][r] is C[32 i + 8 (r / 4) + 4 h + r % 4][32 j + r32]
+  // of the wave tile. Each 32-row block goes through a wave-private LDS
+  // staging area (fp32, rows padded to 136 floats: the two lane halves,
+  // 4 rows apart, land 32 banks apart), then every lane reads V consecutive
+  // columns and the global stores (and residual loads) are 16 bytes per
+  // lane: a few wide VMEM instructions instead of one per (row group,
+  // column block). SwiGLU: the wave's column blocks alternate gate and up
+  // (the 32-row interleave of w_gate_up), block 2p pairs with 2p + 1.
+  constexpr int ROWF = 136;
+  lds_barrier_pinned();  // every wave is done reading operand slots
+  float* stg = (float*)smem + wave * (32 * ROWF);
+  const int rbase = m0 + wm * WT, cbase = n0 + wn * WT;
+  constexpr int V = std::is_same<TC, bf16_t>::value ? 8 : 4;  // columns per lane
+  constexpr int OUT_COLS = EPI == 2 ? WT / 2 : WT;
+  constexpr int LPR = OUT_COLS / V, RPP = 64 / LPR;  // lanes per row, rows per pass
+  const long ldc = EPI == 2 ? N / 2 : N;
+  const long ccol = EPI == 2 ? cbase / 2 : cbase;
+  constexpr int NPASS = 32 / RPP;
+  // residual operand of one pass: V values of row `row` from column `oc`
+  using RRaw = typename std::conditional<std::is_same<TR, float>::value, float4,
+                                         typename std::conditional<V == 8, uint4, uint2>::type>::type;
+  constexpr int RCH = std::is_same<TR, float>::value ? V / 4 : 1;  // RRaw loads per pass
 #pragma unroll
-    for (int i = 0; i < CF::FM; ++i)
+  for (int i = 0; i < Q; ++i) {
+    // residual loads of the whole 32-row block first: issued together, they
+    // overlap (R may alias C, so a load after a store would wait for it);
+    // each element is still read before it is written
+    RRaw rr[EPI == 1 ? NPASS : 1][RCH];
+    if constexpr (EPI == 1) {
 #pragma unroll
-      for (int j = 0; j < CF::FN; ++j)
+      for (int pass = 0; pass < NPASS; ++pass) {
+        const int row = rbase + i * 32 + pass * RPP + lane / LPR, oc = (lane % LPR) * V;
+        const long idx = (long)min(row, M - 1) * ldc + ccol + oc;  // rows past M: a valid row, result unused
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = rbase + i * 16 + 4 * g + r;
-          if (row < M) st_elt<TC>(C, (long)row * N + cbase + j * 16 + c, acc[i][j][r]);
+        for (int q = 0; q < RCH; ++q) rr[pass][q] = *(const RRaw*)(R + idx + q * 4);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < Q; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) stg[(8 * (r >> 2) + 4 * h + (r & 3)) * ROWF + j * 32 + r32] = acc[i][j][r];
+    // LDS accesses of one wave complete in order: the reads below see the writes
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int lr = pass * RPP + lane / LPR, oc = (lane % LPR) * V;
+      const int row = rbase + i * 32 + lr;
+      float v[V];
+      if constexpr (EPI == 2) {
+        const int p = oc / 32, c = oc % 32;
+        const float* g = stg + lr * ROWF + p * 64 + c;
+#pragma unroll
+        for (int e = 0; e < V; e += 4) {
+          const float4 gv = *(const float4*)(g + e), uv = *(const float4*)(g + 32 + e);
+          v[e] = silu_fast(gv.x) * uv.x;
+          v[e + 1] = silu_fast(gv.y) * uv.y;
+          v[e + 2] = silu_fast(gv.z) * uv.z;
+          v[e + 3] = silu_fast(gv.w) * uv.w;
         }
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; e += 4) {
+          const float4 a4 = *(const float4*)(stg + lr * ROWF + oc + e);
+          v[e] = a4.x;
+          v[e + 1] = a4.y;
+          v[e + 2] = a4.z;
+          v[e + 3] = a4.w;
+        }
+      }
+      if constexpr (EPI == 1) {
+        if constexpr (std::is_same<TR, float>::value) {
+#pragma unroll
+          for (int q = 0; q < RCH; ++q) {
+            v[4 * q] += rr[pass][q].x;
+            v[4 * q + 1] += rr[pass][q].y;
+            v[4 * q + 2] += rr[pass][q].z;
+            v[4 * q + 3] += rr[pass][q].w;
+          }
+        } else if constexpr (V == 8) {
+          const uint32_t w4[4] = {rr[pass][0].x, rr[pass][0].y, rr[pass][0].z, rr[pass][0].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += bf_lo(w4[e]);
+            v[2 * e + 1] += bf_hi(w4[e]);
+          }
+        } else {
+          v[0] += bf_lo(rr[pass][0].x);
+          v[1] += bf_hi(rr[pass][0].x);
+          v[2] += bf_lo(rr[pass][0].y);
+          v[3] += bf_hi(rr[pass][0].y);
+        }
+      }
+      if (row >= M) continue;
+      const long idx = (long)row * ldc + ccol + oc;
+      if constexpr (std::is_same<TC, bf16_t>::value) {
+        *(uint4*)(C + idx) = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
+                                        pack_bf2(v[6], v[7]));
+      } else {
+        *(float4*)(C + idx) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
   }
 }
 
@@ -488,7 +492,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
         if constexpr (EPI == 2) {
           const int q = wave >> 1, h = wave & 1;
           const int col = n0 / 2 + 32 * q + 16 * h + c;
-          st_elt<TC>(C, (long)row * (N / 2) + col, silu_f(acc[0][i][r]) * acc[1][i][r]);
+          st_elt<TC>(C, (long)row * (N / 2) + col, silu_fast(acc[0][i][r]) * acc[1][i][r]);
         } else {
 #pragma unroll
           for (int nb = 0; nb < WN; ++nb) {
@@ -529,7 +533,7 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* __restric
         gs += part[((long)s * M + row) * N + gcol];
         us += part[((long)s * M + row) * N + gcol + kGateUpBlock];
       }
-      st_elt<TC>(C, e, silu_f(gs) * us);
+      st_elt<TC>(C, e, silu_fast(gs) * us);
     } else {
       float v = 0.f;
       for (int s = 0; s < S; ++s) v += part[(long)s * M * N + e];
@@ -617,26 +621,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }
 
 // ==================================================================== launch
-// Default prefill tile configuration.
-using TileDefault = TileCfg<256, 256, 64, 2, 4, 2>;  // 8 waves of 128x64, 2 per SIMD
-
-template <class CF, int EPI, typename TR, typename TC>
-int launch_tile_cfg(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
-  constexpr int BM = CF::BM, BN = CF::BN;
-  const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-  constexpr size_t lds = tile_lds_bytes<CF, EPI, TC>();
-  static_assert(lds <= 160 * 1024, "LDS per workgroup");
-  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<CF, EPI, TR, TC>,
-                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr != hipSuccess) return -1;
-  hipLaunchKernelGGL((gemm_tile_kernel<CF, EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(CF::NT), lds, st,
-                     (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n);
-  return 0;
-}
-
 template <int EPI, typename TR, typename TC>
 static int launch_tile(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
-  return launch_tile_cfg<TileDefault, EPI, TR, TC>(M, N, K, A, W, R, C, st);
+  static_assert(tile::LDS_BYTES <= 160 * 1024, "LDS per workgroup");
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<EPI, TR, TC>,
+                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)tile::LDS_BYTES);
+  if (attr != hipSuccess) return -1;
+  const int tiles_m = (M + tile::BM - 1) / tile::BM, tiles_n = N / tile::BN;
+  // wide outputs walk 8 tile-rows per group (more W reuse per XCD), narrow 4
+  const int group = tiles_n >= 64 ? 8 : 4;
+  hipLaunchKernelGGL((gemm_tile_kernel<EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(tile::NT), tile::LDS_BYTES, st,
+                     (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n, group);
+  return 0;
 }
 
 template <int EPI, typename TR, typename TC>
