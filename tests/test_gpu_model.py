@@ -161,48 +161,3 @@ def test_model_rejects_shallow_pool():
     with pytest.raises(B.PsError) as e:
         model.prefill(pool.kv, [s], [4], tok, nxt, ws)
     assert e.value.code == B.PS_E_INVALID
-
-
-def test_70b_layer_fullsize_prefill_and_decode():
-    """One 70B-shaped layer (d 8192, 64/8 heads, F 28672): a 256-token prompt
-    and a decode step of 4 sequences at context 4096."""
-    wl = CONFIGS["llama70b_model"]
-    sh = wl.shape
-    w = gen.layer_weights(wl, 0)
-    wf = H.weights_f64(w, "bf16")
-    dev = H.DeviceLayer(w, "bf16")
-    ctx = [4096, 4095, 3000, 17]
-    pool = H.Pool(sh, sum((c + 16) // 16 for c in ctx) + 32, 8, 260, seed=5)
-    kv = pool.kv
-    layer = B.Layer(pool.cfg)
-    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, 256, 8, 260))
-    g = torch.Generator(device="cuda").manual_seed(99)
-    seqs, hist = [], []
-    for c in ctx:
-        s = kv.open()
-        kv.alloc(s, c + 1)
-        k = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
-        v = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
-        kv.append(0, [s], [c], k, v, ws)
-        kv.commit([s], [c])
-        seqs.append(s)
-        hist.append((H.to_f64(k), H.to_f64(v)))
-    x = gen.decode_input(wl, len(ctx), 0)
-    out = H.empty((len(ctx), sh.hidden), "bf16")
-    layer.decode_step(dev.w, kv, 0, B.PS_PHASE_ANSWER, seqs, H.to_dev(x, "bf16"), out, ws)
-    sync()
-    got = H.to_f64(out)
-    xf = gen.widen(x, "bf16")
-    for b in range(len(ctx)):
-        ref = O.layer_sequence(wf, sh, xf[b:b + 1], *hist[b])["out"][0]
-        mx, rms = H.normwise(got[b], ref)
-        assert mx <= H.NORMWISE_TOL_70B and rms <= H.NORMWISE_TOL_70B, f"decode b={b}: {mx:.2e} {rms:.2e}"
-    p = kv.open()
-    kv.alloc(p, 256)
-    xp = gen.prefill_input(wl, 256)
-    outp = H.empty((256, sh.hidden), "bf16")
-    layer.prefill(dev.w, kv, 0, [p], [256], H.to_dev(xp, "bf16"), outp, ws)
-    sync()
-    ref = O.layer_sequence(wf, sh, gen.widen(xp, "bf16"))["out"]
-    mx, rms = H.normwise(H.to_f64(outp), ref)
-    assert mx <= H.NORMWISE_TOL_70B and rms <= H.NORMWISE_TOL_70B, f"prefill: {mx:.2e} {rms:.2e}"
