@@ -672,9 +672,12 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
   int bad = 0;
   bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st);
-  bad |= launch_gemm(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes, st);
+  // decode-sized QKV: RoPE + KV write sums the split-K partials itself
+  int s_qkv = 1;
+  bad |= launch_gemm_split(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes,
+                           st, &s_qkv);
   bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + P.o_fr), P.n_seqs, c.n_q_heads,
-                             c.n_kv_heads, c.head_dim, st);
+                             c.n_kv_heads, c.head_dim, st, (const float*)gws, s_qkv);
   // attention: prefill rows on the flash kernel, decode rows on the split-K
   // kernel, anything else (fp32, other head sizes) on the vector kernel
   if (P.n_chunk > 0) {
@@ -697,8 +700,18 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
                                  pool, si, bt, o, scale, st);
     }
   }
-  bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
-  bad |= launch_rmsnorm(PS_F32, dt, dt, rows, d, h, w->ffn_norm, c.rms_eps, xn, st);
+  // decode-sized O projection: one kernel sums the split-K partials, adds the
+  // residual, stores h and normalises it
+  int s_o = 1;
+  if (dt == PS_BF16)
+    bad |= launch_gemm_split(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st, &s_o);
+  else
+    bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
+  if (s_o > 1)
+    bad |= launch_split_residual_rmsnorm(rows, d, s_o, (const float*)gws, x_in, (float*)h, w->ffn_norm, c.rms_eps, xn,
+                                         st);
+  else
+    bad |= launch_rmsnorm(PS_F32, dt, dt, rows, d, h, w->ffn_norm, c.rms_eps, xn, st);
   bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes, st);
   bad |= launch_gemm(dt, PS_F32, dt, PS_EPI_RESIDUAL, rows, d, c.ffn, m, w->w_down, h, x_out, gws, gws_bytes, st);
   return bad;

@@ -783,6 +783,37 @@ int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, con
   return -1;
 }
 
+// launch_gemm, except that a decode-sized bf16 GEMM whose plan splits K in
+// 2, 4 or 8 stops at the split partials (fp32 [S][M][N] at the head of ws,
+// summed in split order by the consumer, which fuses the reduction with its
+// own work); *splits = S then, else 1 and C holds the result.
+int launch_gemm_split(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
+                      const void* R, void* C, void* ws, size_t ws_bytes, hipStream_t st, int* splits) {
+  *splits = 1;
+  if (dtype == 1 && M > 0 && M <= skinny::MAXM && N % 64 == 0 && K % 64 == 0 && epi != 2) {
+    const SkinnyPlan pl = gemm_skinny_plan(M, N, K);
+    if (pl.s == 2 || pl.s == 4 || pl.s == 8) {  // the split counts the fused consumers take
+      if (ws_bytes < gemm_workspace_bytes(dtype, M, N, K)) return -2;
+      *splits = pl.s;
+      float* part = (float*)ws;
+      // the partial kernel's output does not depend on the epilogue or the
+      // output types (only its weight-row mapping does, for SwiGLU)
+      auto go = [&](auto mbc) {
+        constexpr int MB = decltype(mbc)::value;
+        if (pl.wn == 2) return launch_skinny_k<MB, 2, 0, float, float, false>(M, N, K, pl.s, A, W, part, R, C, st);
+        return launch_skinny_k<MB, 1, 0, float, float, false>(M, N, K, pl.s, A, W, part, R, C, st);
+      };
+      switch ((M + 15) / 16) {
+        case 1: return go(std::integral_constant<int, 1>{});
+        case 2: return go(std::integral_constant<int, 2>{});
+        case 3: return go(std::integral_constant<int, 3>{});
+        default: return go(std::integral_constant<int, 4>{});
+      }
+    }
+  }
+  return launch_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, W, R, C, ws, ws_bytes, st);
+}
+
 }  // namespace ps
 
 namespace ps {

@@ -33,32 +33,17 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TX* __restrict__ x, 
   }
 }
 
-// Vectorised bf16 -> bf16 variant: 8 elements per 16-byte access, the row
-// kept in registers between the two passes (d <= 256 * 8 * VPT).
-template <typename TX, int VPT>
-__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const TX* __restrict__ x, const bf16_t* __restrict__ g,
-                                                          bf16_t* __restrict__ y, int d, float eps) {
-  const long row = blockIdx.x;
-  float v[VPT][8];
+// Second half of the vectorised RMSNorm, shared by the kernels that hold a
+// row in registers (v[c][e] = element (c * 256 + threadIdx.x) * 8 + e):
+// sum of squares in that order, wave then workgroup reduction, bf16 output.
+template <int VPT>
+__device__ __forceinline__ void rmsnorm_row_out(const float (&v)[VPT][8], const bf16_t* __restrict__ g,
+                                                bf16_t* __restrict__ yr, int d, float eps) {
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < VPT; ++c) {
-    int i = (c * 256 + threadIdx.x) * 8;
+    const int i = (c * 256 + threadIdx.x) * 8;
     if (i < d) {
-      if constexpr (sizeof(TX) == 2) {
-        uint4 w = *(const uint4*)(x + row * d + i);
-        uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[c][2 * e] = bf_lo(ws[e]);
-          v[c][2 * e + 1] = bf_hi(ws[e]);
-        }
-      } else {
-        float4 a = *(const float4*)(x + row * d + i);
-        float4 b = *(const float4*)(x + row * d + i + 4);
-        v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
-        v[c][4] = b.x; v[c][5] = b.y; v[c][6] = b.z; v[c][7] = b.w;
-      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) ss += v[c][e] * v[c][e];
     }
@@ -79,9 +64,111 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const TX* __restrict__
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         o[e] = pack_bf2(v[c][2 * e] * inv * bf_lo(gs[e]), v[c][2 * e + 1] * inv * bf_hi(gs[e]));
-      *(uint4*)(y + row * d + i) = make_uint4(o[0], o[1], o[2], o[3]);
+      *(uint4*)(yr + i) = make_uint4(o[0], o[1], o[2], o[3]);
     }
   }
+}
+
+// Vectorised bf16 -> bf16 variant: 8 elements per 16-byte access, the row
+// kept in registers between the two passes (d <= 256 * 8 * VPT).
+template <typename TX, int VPT>
+__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const TX* __restrict__ x, const bf16_t* __restrict__ g,
+                                                          bf16_t* __restrict__ y, int d, float eps) {
+  const long row = blockIdx.x;
+  float v[VPT][8];
+#pragma unroll
+  for (int c = 0; c < VPT; ++c) {
+    int i = (c * 256 + threadIdx.x) * 8;
+    if (i < d) {
+      if constexpr (sizeof(TX) == 2) {
+        uint4 w = *(const uint4*)(x + row * d + i);
+        uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[c][2 * e] = bf_lo(ws[e]);
+          v[c][2 * e + 1] = bf_hi(ws[e]);
+        }
+      } else {
+        float4 a = *(const float4*)(x + row * d + i);
+        float4 b = *(const float4*)(x + row * d + i + 4);
+        v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
+        v[c][4] = b.x; v[c][5] = b.y; v[c][6] = b.z; v[c][7] = b.w;
+      }
+    }
+  }
+  rmsnorm_row_out<VPT>(v, g, y + row * d, d, eps);
+}
+
+// Decode-sized O projection fused with its consumer: h = sum of the split-K
+// partials of o W^T, in split order, + the residual x (bf16), stored fp32;
+// then hn = RMSNorm(h) * g from the same registers. The sum and the norm
+// are those of the separate reduce and RMSNorm kernels, bit for bit.
+template <int VPT, int S>
+__global__ __launch_bounds__(256) void split_residual_rmsnorm_kernel(const float* __restrict__ part, long mn,
+                                                                     const bf16_t* __restrict__ res,
+                                                                     float* __restrict__ h,
+                                                                     const bf16_t* __restrict__ g,
+                                                                     bf16_t* __restrict__ y, int d, float eps) {
+  const long row = blockIdx.x;
+  float v[VPT][8];
+  // every partial and residual load of the row is issued before the sums
+  // (S is a compile-time count): one round of memory latency, not S x VPT
+  float4 pa[VPT][S][2];
+  uint4 rw[VPT];
+#pragma unroll
+  for (int c = 0; c < VPT; ++c) {
+    const int i = (c * 256 + threadIdx.x) * 8;
+    if (i < d) {
+      const long off = row * d + i;
+#pragma unroll
+      for (int sp = 0; sp < S; ++sp) {
+        pa[c][sp][0] = *(const float4*)(part + sp * mn + off);
+        pa[c][sp][1] = *(const float4*)(part + sp * mn + off + 4);
+      }
+      rw[c] = *(const uint4*)(res + off);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < VPT; ++c) {
+    const int i = (c * 256 + threadIdx.x) * 8;
+    if (i < d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < S; ++sp) {
+        v[c][0] += pa[c][sp][0].x; v[c][1] += pa[c][sp][0].y; v[c][2] += pa[c][sp][0].z; v[c][3] += pa[c][sp][0].w;
+        v[c][4] += pa[c][sp][1].x; v[c][5] += pa[c][sp][1].y; v[c][6] += pa[c][sp][1].z; v[c][7] += pa[c][sp][1].w;
+      }
+      const uint32_t rs[4] = {rw[c].x, rw[c].y, rw[c].z, rw[c].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[c][2 * e] += bf_lo(rs[e]);
+        v[c][2 * e + 1] += bf_hi(rs[e]);
+      }
+      const long off = row * d + i;
+      *(float4*)(h + off) = make_float4(v[c][0], v[c][1], v[c][2], v[c][3]);
+      *(float4*)(h + off + 4) = make_float4(v[c][4], v[c][5], v[c][6], v[c][7]);
+    }
+  }
+  rmsnorm_row_out<VPT>(v, g, y + row * d, d, eps);
+}
+
+int launch_split_residual_rmsnorm(int rows, int d, int S, const float* part, const void* res, float* h,
+                                  const void* g, float eps, void* y, hipStream_t st) {
+  if (rows == 0) return 0;
+  if (d % 8 != 0 || d > 256 * 8 * 4) return -1;
+  const long mn = (long)rows * d;
+#define SRR_CASE(S_)                                                                                        \
+  if (S == S_) {                                                                                            \
+    hipLaunchKernelGGL((split_residual_rmsnorm_kernel<4, S_>), dim3(rows), dim3(256), 0, st, part, mn,       \
+                       (const bf16_t*)res, h, (const bf16_t*)g, (bf16_t*)y, d, eps);                        \
+    return 0;                                                                                               \
+  }
+  SRR_CASE(2)
+  SRR_CASE(4)
+  SRR_CASE(8)
+#undef SRR_CASE
+  return -1;
 }
 
 int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
@@ -155,12 +242,18 @@ __device__ __forceinline__ int find_seq_wave(const SeqInfo* __restrict__ si, int
 // One row per workgroup: rotate the row's q and k heads (rotate-half, angle
 // pos * inv_freq[j] evaluated in fp64), write q to q_out and k, v into the
 // row's page slot. bf16 rows move four pairs per thread with 8-byte accesses.
-template <typename T>
+// PART (bf16, decode): the QKV row is not materialised; it is the sum of the
+// GEMM's S split-K partials (fp32 [S][rows][n_q + 2 n_kv][hd]) in split order,
+// rounded to bf16, exactly what the separate reduce kernel would have stored.
+template <typename T, int SS>
 __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__ qkv, T* __restrict__ q_out,
                                                            T* __restrict__ pool, const SeqInfo* __restrict__ si,
                                                            const int32_t* __restrict__ bt,
                                                            const double* __restrict__ inv_freq, int n_seqs,
-                                                           int n_q, int n_kv, int hd) {
+                                                           int n_q, int n_kv, int hd, const float* __restrict__ part,
+                                                           long mn) {
+  constexpr bool PART = SS > 0;  // SS split-K partials, a compile-time count
+  static_assert(!PART || std::is_same<T, bf16_t>::value, "split partials feed the bf16 path");
   const int row = blockIdx.x;
   const int half = hd >> 1;
   __shared__ float cs[64], sn[64];
@@ -182,6 +275,37 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   __syncthreads();
   const int dqkv = (n_q + 2 * n_kv) * hd;
   const T* xr = qkv + (long)row * dqkv;
+  const float* pr = PART ? part + (long)row * dqkv : nullptr;  // partials of this row
+  // four consecutive elements of the row from column col (col % 4 == 0)
+  auto load4 = [&](int col, float (&x)[4]) {
+    if constexpr (PART) {
+      float4 p4[SS > 0 ? SS : 1];
+#pragma unroll
+      for (int sp = 0; sp < SS; ++sp) p4[sp] = *(const float4*)(pr + sp * mn + col);
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int sp = 0; sp < SS; ++sp) {
+        acc.x += p4[sp].x; acc.y += p4[sp].y; acc.z += p4[sp].z; acc.w += p4[sp].w;
+      }
+      x[0] = bf2f(f2bf(acc.x)); x[1] = bf2f(f2bf(acc.y)); x[2] = bf2f(f2bf(acc.z)); x[3] = bf2f(f2bf(acc.w));
+    } else {
+      const uint2 a = *(const uint2*)(xr + col);
+      x[0] = bf_lo(a.x); x[1] = bf_hi(a.x); x[2] = bf_lo(a.y); x[3] = bf_hi(a.y);
+    }
+  };
+  auto load1 = [&](int col) -> float {
+    if constexpr (PART) {
+      float p1[SS > 0 ? SS : 1];
+#pragma unroll
+      for (int sp = 0; sp < SS; ++sp) p1[sp] = pr[sp * mn + col];
+      float acc = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < SS; ++sp) acc += p1[sp];
+      return bf2f(f2bf(acc));
+    } else {
+      return Elt<T>::load(xr, col);
+    }
+  };
   const int page = bt[s.bt_off + pos / kPageTokens];
   const int slot = pos % kPageTokens;
   auto dst_of = [&](int head) -> T* {  // start of the head's rotated row
@@ -195,10 +319,9 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
     const int quads = half / 4;
     for (int idx = threadIdx.x; idx < (n_q + n_kv) * quads; idx += blockDim.x) {
       const int head = idx / quads, j = (idx - head * quads) * 4;
-      const uint2 a = *(const uint2*)(xr + head * hd + j);
-      const uint2 c = *(const uint2*)(xr + head * hd + j + half);
-      const float x1[4] = {bf_lo(a.x), bf_hi(a.x), bf_lo(a.y), bf_hi(a.y)};
-      const float x2[4] = {bf_lo(c.x), bf_hi(c.x), bf_lo(c.y), bf_hi(c.y)};
+      float x1[4], x2[4];
+      load4(head * hd + j, x1);
+      load4(head * hd + j + half, x2);
       float y1[4], y2[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -212,32 +335,59 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   } else {
     for (int idx = threadIdx.x; idx < (n_q + n_kv) * half; idx += blockDim.x) {
       int head = idx / half, j = idx - head * half;
-      float x1 = Elt<T>::load(xr, head * hd + j);
-      float x2 = Elt<T>::load(xr, head * hd + j + half);
+      float x1 = load1(head * hd + j);
+      float x2 = load1(head * hd + j + half);
       T* d = dst_of(head);
       Elt<T>::store(d, j, x1 * cs[j] - x2 * sn[j]);
       Elt<T>::store(d, j + half, x2 * cs[j] + x1 * sn[j]);
     }
   }
   // v: stored dimension-major within the page
-  for (int idx = threadIdx.x; idx < n_kv * hd; idx += blockDim.x) {
-    int kvh = idx / hd, dim = idx - kvh * hd;
-    T v = xr[(n_q + n_kv) * hd + idx];
-    pool[kv_block(page, kvh, n_kv, hd) + (long)kPageTokens * hd + (long)dim * kPageTokens + slot] = v;
+  if constexpr (PART) {
+    // four consecutive dimensions per thread (hd % 4 == 0 on the bf16 path)
+    for (int idx = threadIdx.x * 4; idx < n_kv * hd; idx += blockDim.x * 4) {
+      const int kvh = idx / hd, dim = idx - kvh * hd;
+      float x4[4];
+      load4((n_q + n_kv) * hd + idx, x4);
+      T* vb = pool + kv_block(page, kvh, n_kv, hd) + (long)kPageTokens * hd + slot;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vb[(long)(dim + e) * kPageTokens] = f2bf(x4[e]);
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < n_kv * hd; idx += blockDim.x) {
+      int kvh = idx / hd, dim = idx - kvh * hd;
+      T v = xr[(n_q + n_kv) * hd + idx];
+      pool[kv_block(page, kvh, n_kv, hd) + (long)kPageTokens * hd + (long)dim * kPageTokens + slot] = v;
+    }
   }
 }
 
 int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* pool_layer, const SeqInfo* si,
                         const int32_t* bt, const double* inv_freq, int n_seqs, int n_q, int n_kv, int hd,
-                        hipStream_t st) {
+                        hipStream_t st, const float* part, int splits) {
   if (rows == 0) return 0;
   if (hd > 128) return -1;
+  const long mn = (long)rows * (n_q + 2 * n_kv) * hd;
+  if (part && splits > 1) {
+    if (dt != 1 || hd % 8 != 0) return -1;
+#define ROPE_PART_CASE(S_)                                                                                      \
+    if (splits == S_) {                                                                                         \
+      hipLaunchKernelGGL((rope_kvwrite_kernel<bf16_t, S_>), dim3(rows), dim3(256), 0, st, (const bf16_t*)qkv,   \
+                         (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd, part, mn); \
+      return 0;                                                                                                 \
+    }
+    ROPE_PART_CASE(2)
+    ROPE_PART_CASE(4)
+    ROPE_PART_CASE(8)
+#undef ROPE_PART_CASE
+    return -1;
+  }
   if (dt == 1)
-    hipLaunchKernelGGL(rope_kvwrite_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, (const bf16_t*)qkv,
-                       (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd);
+    hipLaunchKernelGGL((rope_kvwrite_kernel<bf16_t, 0>), dim3(rows), dim3(256), 0, st, (const bf16_t*)qkv,
+                       (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd, nullptr, 0L);
   else
-    hipLaunchKernelGGL(rope_kvwrite_kernel<float>, dim3(rows), dim3(256), 0, st, (const float*)qkv,
-                       (float*)q_out, (float*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd);
+    hipLaunchKernelGGL((rope_kvwrite_kernel<float, 0>), dim3(rows), dim3(256), 0, st, (const float*)qkv,
+                       (float*)q_out, (float*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd, nullptr, 0L);
   return 0;
 }
 

@@ -13,9 +13,13 @@ namespace ps {
 int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
                    void* y, hipStream_t st);
 
+// part/splits: when splits > 1 (bf16), the QKV rows are the sum of `splits`
+// fp32 split-K partials at part (see launch_gemm_split), qkv is not read
 int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* pool_layer, const SeqInfo* si,
                         const int32_t* bt, const double* inv_freq, int n_seqs, int n_q, int n_kv, int hd,
-                        hipStream_t st);
+                        hipStream_t st, const float* part = nullptr, int splits = 1);
+int launch_split_residual_rmsnorm(int rows, int d, int S, const float* part, const void* res, float* h,
+                                  const void* g, float eps, void* y, hipStream_t st);
 int launch_kv_append(int dt, int rows, const void* k, const void* v, void* pool_layer, const SeqInfo* si,
                      const int32_t* bt, int n_seqs, int n_kv, int hd, hipStream_t st);
 int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt, void* k_out, void* v_out,
@@ -36,6 +40,8 @@ int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* p
 int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
                 const void* R, void* C, void* ws, size_t ws_bytes, hipStream_t st);
 size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
+int launch_gemm_split(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
+                      const void* R, void* C, void* ws, size_t ws_bytes, hipStream_t st, int* splits);
 struct SkinnyPlan {
   int wn;  // 64-row weight blocks per workgroup (1 or 2)
   int s;   // K splits

@@ -189,3 +189,66 @@ def test_layer_rejects_capacity_overrun_without_launching(h8):
     assert e.value.code == B.PS_E_CAPACITY
     assert h.kv.seq_len(s) == 0
     h.kv.free(s)
+
+
+@pytest.mark.parametrize("batch", [64, 37])
+def test_8b_decode_step_equals_composed_stage_ops_bit_for_bit(h8, batch):
+    """ps_decode_step against the same stages called one by one through the
+    single-op entry points (norm, QKV GEMM, RoPE + KV write, split-K
+    attention, O GEMM + residual, norm, gate_up + SwiGLU, down + residual) on
+    a second pool holding the same history: the layer's fused kernels must
+    reproduce the composed path exactly, output and written K/V."""
+    h = h8
+    sh, wl = h.shape, h.wl
+    d, dq, dkv, F = sh.hidden, sh.n_q * sh.head_dim, sh.n_kv * sh.head_dim, sh.ffn
+    ctx = [40 + (37 * i) % 160 for i in range(batch)]
+    pools = [H.Pool(sh, sum((c + 16) // 16 for c in ctx) + 8, batch, 16, seed=11) for _ in range(2)]
+    ws = H.workspace(B.Layer.workspace_bytes(pools[0].cfg, 64, batch, 16))
+    g = torch.Generator(device="cuda").manual_seed(123)
+    seqs = [[], []]
+    for c in ctx:
+        k = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        for p, ss in zip(pools, seqs):
+            s = p.kv.open()
+            p.kv.alloc(s, c + 1)
+            p.kv.append(0, [s], [c], k, v, ws)
+            p.kv.commit([s], [c])
+            ss.append(s)
+    x = H.to_dev(gen.decode_input(wl, batch, 3), "bf16")
+    out_layer = H.empty((batch, d), "bf16")
+    h.layer.decode_step(h.dev.w, pools[0].kv, 0, B.PS_PHASE_ANSWER, seqs[0], x, out_layer, ws)
+    sync()
+    t = h.dev.t
+    bf, f32 = B.PS_BF16, B.PS_F32
+    xn = H.empty((batch, d), "bf16")
+    qkv = H.empty((batch, dq + 2 * dkv), "bf16")
+    q = H.empty((batch, dq), "bf16")
+    o = H.empty((batch, dq), "bf16")
+    hh = H.empty((batch, d), "f32")
+    hn = H.empty((batch, d), "bf16")
+    m = H.empty((batch, F), "bf16")
+    out_ops = H.empty((batch, d), "bf16")
+    kv2 = pools[1].kv
+    B.op_rmsnorm(bf, bf, bf, batch, d, x, t["attn_norm"], sh.eps, xn)
+    B.op_gemm(bf, 0, bf, B.PS_EPI_STORE, batch, dq + 2 * dkv, d, xn, t["w_qkv"], None, qkv, ws)
+    B.op_rope_kvwrite(kv2, 0, seqs[1], [1] * batch, qkv, q, ws)
+    B.op_decode_attention(kv2, 0, seqs[1], q, o, ws)
+    B.op_gemm(bf, bf, f32, B.PS_EPI_RESIDUAL, batch, d, dq, o, t["w_o"], x, hh, ws)
+    B.op_rmsnorm(f32, bf, bf, batch, d, hh, t["ffn_norm"], sh.eps, hn)
+    B.op_gemm(bf, 0, bf, B.PS_EPI_SWIGLU, batch, 2 * F, d, hn, t["w_gate_up"], None, m, ws)
+    B.op_gemm(bf, f32, bf, B.PS_EPI_RESIDUAL, batch, d, F, m, t["w_down"], hh, out_ops, ws)
+    sync()
+    np.testing.assert_array_equal(H.bits(out_layer), H.bits(out_ops))
+    for p, ss in zip(pools, seqs):
+        p.kv.commit(ss, [1] * batch)
+    for i in (0, batch // 2, batch - 1):  # the K/V row each path wrote at position ctx
+        got = []
+        for p, ss in zip(pools, seqs):
+            k = H.empty((ctx[i] + 1, sh.n_kv, sh.head_dim), "bf16")
+            v = H.empty((ctx[i] + 1, sh.n_kv, sh.head_dim), "bf16")
+            p.kv.gather(0, ss[i], k, v, ws)
+            got.append((k[-1], v[-1]))
+        sync()
+        np.testing.assert_array_equal(H.bits(got[0][0]), H.bits(got[1][0]))
+        np.testing.assert_array_equal(H.bits(got[0][1]), H.bits(got[1][1]))
