@@ -365,8 +365,12 @@ int32_t choose_split_pages(const std::vector<SeqInfo>& si, size_t first, int n_k
   (void)phase;
   long total = 0;
   for (size_t b = first; b < si.size(); ++b) total += (si[b].kv_before + si[b].n_new + 15) / 16;
-  // about 3072 workgroups over the chip (a dozen per CU), at least 8 pages per split
-  const long target_items = std::max(1, 3072 / std::max(1, n_kv));
+  // about 1024 workgroups over the chip (two rounds of the 512 that fit at
+  // two per CU), at least 8 pages per split. Measured over split sizes on
+  // the 8B decode and think and the 70B decode workloads: every workgroup
+  // pays a ramp-up (its first pages' latency) and a merge, so fewer, longer
+  // splits stream faster down to ~1000 workgroups (3072: 5-10% slower).
+  const long target_items = std::max(1, 1024 / std::max(1, n_kv));
   long sp = (total + target_items - 1) / target_items;
   sp = std::max<long>(sp, 8);
   sp = (sp + 3) / 4 * 4;
@@ -389,11 +393,13 @@ DecodePlan plan_decode(const std::vector<SeqInfo>& si, size_t first, int32_t spl
     const int32_t ns = (np + split_pages - 1) / split_pages;
     p.part_begin.push_back(p.n_parts);
     p.part_count.push_back(ns);
+    // ns splits of at most split_pages pages, as even as possible (sizes
+    // differ by at most one page), so no short remainder split trails
     for (int32_t k = 0; k < ns; ++k) {
       DecodeItem it;
       it.b = (int32_t)(b - first);
-      it.page_begin = k * split_pages;
-      it.page_end = std::min(np, (k + 1) * split_pages);
+      it.page_begin = (int32_t)((long)k * np / ns);
+      it.page_end = (int32_t)((long)(k + 1) * np / ns);
       it.part = p.n_parts + k;
       p.items.push_back(it);
     }
