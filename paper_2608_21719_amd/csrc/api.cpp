@@ -679,9 +679,13 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
   int bad = 0;
   bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st);
   // decode-sized QKV: RoPE + KV write sums the split-K partials itself
+  // (bf16, head_dim a multiple of 8: the fused reader's vector width)
   int s_qkv = 1;
-  bad |= launch_gemm_split(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes,
-                           st, &s_qkv);
+  if (dt == PS_BF16 && c.head_dim % 8 == 0)
+    bad |= launch_gemm_split(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws,
+                             gws_bytes, st, &s_qkv);
+  else
+    bad |= launch_gemm(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes, st);
   bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + P.o_fr), P.n_seqs, c.n_q_heads,
                              c.n_kv_heads, c.head_dim, st, (const float*)gws, s_qkv);
   // attention: prefill rows on the flash kernel, decode rows on the split-K
@@ -708,8 +712,9 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
   }
   // decode-sized O projection: one kernel sums the split-K partials, adds the
   // residual, stores h and normalises it
+  // (bf16, d a multiple of 8 up to 8192: a row fits the fused kernel's registers)
   int s_o = 1;
-  if (dt == PS_BF16)
+  if (dt == PS_BF16 && d % 8 == 0 && d <= 8192)
     bad |= launch_gemm_split(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st, &s_o);
   else
     bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
