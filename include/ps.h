@@ -262,7 +262,7 @@ ps_status ps_op_rmsnorm(int32_t x_dtype, int32_t g_dtype, int32_t y_dtype, int32
  *                    silu(gate) * up with gate/up the de-interleaved halves
  * Decode-sized M (<= 64) splits K across workgroups and needs ws of at least
  * ps_op_gemm_workspace_bytes for its fp32 partials (0 bytes otherwise).
- * Supported: bf16 with K % 64 == 0 and N % 256 == 0 (or M <= 64 and
+ * Supported: bf16 with K % 64 == 0, K < 2^21 and N % 256 == 0 (or M <= 64 and
  * N % 64 == 0); fp32 any shape; SwiGLU needs N % 64 == 0. */
 #define PS_EPI_STORE 0
 #define PS_EPI_RESIDUAL 1

@@ -51,6 +51,20 @@ __device__ __forceinline__ void load_lds16(const bf16_t* g, bf16_t* lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
+// The same fill through a buffer resource (buffer_load_dwordx4 ... lds):
+// `voffset` is the lane's byte offset from the resource base. The compiler
+// counts this form on vmcnt alone, so LDS reads issued around it keep exact
+// lgkmcnt waits; around the FLAT form above it waits for every outstanding
+// LDS read (lgkmcnt(0)) before each use of a fragment.
+__device__ __forceinline__ void load_lds16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
+}
+// Raw (stride 0) buffer resource over `bytes` bytes from `base`; loads past
+// the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 // s_waitcnt vmcnt(n) lgkmcnt(0): this wave's global->LDS fills older than
 // its n most recent have landed, and its own LDS reads have returned.
 template <int N>
@@ -73,27 +87,37 @@ __device__ __forceinline__ void lds_barrier_pinned() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
+// f(std::integral_constant<int, i>) for i = B .. E-1, unrolled at compile
+// time (register arrays indexed by i stay in registers).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // ====================================================================== tile
 // Prefill-sized M. Workgroup tile 256 x 256, four waves of 128 x 128 (one
 // per SIMD), v_mfma_f32_32x32x16_bf16 with the 256 accumulators per lane in
 // AGPRs. K runs in 64-wide stages through two LDS slots (128 KiB) filled by
-// global->LDS DMA; LDS rows are 128 B, their 16-byte chunks XOR-swizzled by
-// (row / 2) % 8 so that the operand reads of 16 consecutive rows hit 16
-// distinct bank groups (the DMA lane addresses are chosen so that the
-// linear fill lands swizzled).
+// global->LDS DMA (buffer form); LDS rows are 128 B, their 16-byte chunks
+// XOR-swizzled by (row / 2) % 8 so that the operand reads of 16 consecutive
+// rows hit 16 distinct bank groups (the DMA lane addresses are chosen so
+// that the linear fill lands swizzled).
 //
-// Schedule of stage st (slot st & 1), four 16-k slices of 16 MFMAs each:
-//  * slices 0..2: after two MFMAs, read the next slice's fragments in one
-//    burst (the compiler waits for every outstanding LDS read before the
-//    first MFMA that uses a fragment, so a burst issued early has ~14 MFMAs
-//    to land); slices 0 and 1 also issue the second part of the DMA of
-//    stage st+1;
-//  * wait for stage st+1 and this stage's reads, one barrier;
-//  * slice 3: read stage st+1's first fragments, and issue the first part
-//    of stage st+2's DMA into slot st & 1, whose last reads are complete.
-// Spreading a stage's 16 DMA instructions per wave over three slices keeps
-// the address unit from backing up: issued as one burst they stall the
-// waves' instruction streams (the cost was per instruction, not per byte).
+// Schedule of stage st (slot st & 1), four 16-k slices of 16 MFMAs each.
+// Every slice interleaves with its MFMAs:
+//  * the reads of the next slice's eight fragments, one after each of the
+//    first eight MFMAs, in the order the next slice first uses them
+//    (a0 b0 b1 b2 b3 a1 a2 a3), so its MFMAs wait only for their own;
+//  * DMA instructions, one after every other MFMA from the second: in
+//    slices 0 and 1 the rest of stage st+1, in slice 3 the first part of
+//    stage st+2 into slot st & 1.
+// After slice 2: wait for stage st+1 and this stage's reads, one barrier
+// (slot st & 1 is free from there, and slice 3 reads stage st+1's first
+// fragments). Issued in bursts, DMA or reads back up the address unit and
+// the LDS queue and stall the waves' instruction streams.
 namespace tile {
 constexpr int BM = 256, BN = 256, BK = 64, NT = 256, WT = 128;
 constexpr int CPR = BK / 8, RPL = 64 / CPR;                         // 8 chunks per row, 8 rows per DMA
@@ -101,6 +125,9 @@ constexpr int A_ELTS = BM * BK, STAGE = (BM + BN) * BK;             // bf16 elem
 constexpr int A_LOADS = BM / RPL / 4, B_LOADS = BN / RPL / 4, LOADS = A_LOADS + B_LOADS;  // per wave
 constexpr int Q = WT / 32;                                           // 4 x 4 blocks of 32 x 32
 constexpr int D3 = 6, D0 = 5, D1 = LOADS - D3 - D0;                  // DMA split over slices 3, 0, 1
+constexpr int DMA_AT = 1, DMA_EVERY = 2;                             // after MFMAs 1, 3, 5, ...
+static_assert(DMA_AT + (D3 - 1) * DMA_EVERY < Q * Q && DMA_AT + (D0 - 1) * DMA_EVERY < Q * Q &&
+                  DMA_AT + (D1 - 1) * DMA_EVERY < Q * Q, "DMA slots in a slice");
 constexpr size_t LDS_BYTES = 2 * (size_t)STAGE * 2;
 __device__ __forceinline__ int swz(int row, int ch) { return row * BK + ((ch ^ ((row >> 1) & 7)) << 3); }
 }  // namespace tile
@@ -129,42 +156,47 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  // DMA sources: a workgroup-uniform base plus a 32-bit lane offset (elements)
+  // DMA sources: buffer resources at the tile's A rows and W blocks, 32-bit
+  // lane byte offsets (rows past M read row M-1, results unused)
   const int lrow = lane / CPR, lpos = lane % CPR;
   uint32_t aoff[A_LOADS], boff[B_LOADS];
 #pragma unroll
   for (int i = 0; i < A_LOADS; ++i) {
     const int row = (wave * A_LOADS + i) * RPL + lrow;
-    aoff[i] = (uint32_t)(min(m0 + row, M - 1) - m0) * K + (lpos ^ ((row >> 1) & 7)) * 8;
+    aoff[i] = ((uint32_t)(min(m0 + row, M - 1) - m0) * K + (lpos ^ ((row >> 1) & 7)) * 8) * 2;
   }
 #pragma unroll
   for (int i = 0; i < B_LOADS; ++i) {  // tiled W: rows of 64-row block row/64, k-tile added per stage
     const int row = (wave * B_LOADS + i) * RPL + lrow;
-    boff[i] = (uint32_t)(row >> 6) * (K / 64) * kWTileElts + (row & 63) * 64 + (lpos ^ ((row >> 1) & 7)) * 8;
+    boff[i] = ((uint32_t)(row >> 6) * (K / 64) * kWTileElts + (row & 63) * 64 + (lpos ^ ((row >> 1) & 7)) * 8) * 2;
   }
-  const bf16_t* Ablk = A + (long)m0 * K;
-  const bf16_t* Wblk = W + (long)(n0 >> 6) * (K / 64) * kWTileElts;
   static_assert(BK == kWTile, "one W tile per stage");
+  const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(A + (long)m0 * K, (uint32_t)min(M - m0, BM) * K * 2);
+  const __amdgpu_buffer_rsrc_t rW =
+      buffer_rsrc(W + (long)(n0 >> 6) * (K / 64) * kWTileElts, (uint32_t)(BN / 64) * (K / 64) * kWTileElts * 2);
   // DMA instruction l (0..LOADS-1) of stage s into slot s & 1
-  auto dma = [&](int s, int l) {
+  auto dma = [&](int s, int l) __attribute__((always_inline)) {
     bf16_t* st = smem + (s & 1) * STAGE;
     if (l < A_LOADS)
-      load_lds16(Ablk + s * BK + aoff[l], st + (wave * A_LOADS + l) * RPL * BK);
+      load_lds16_buf(rA, aoff[l] + s * BK * 2, st + (wave * A_LOADS + l) * RPL * BK);
     else
-      load_lds16(Wblk + (long)s * kWTileElts + boff[l - A_LOADS], st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
+      load_lds16_buf(rW, boff[l - A_LOADS] + s * kWTileElts * 2, st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
   };
 
   // 32x32x16 operands: lane (h, r) holds row r of a 32-row block, k 8h..8h+7
   // of a 16-k slice; fragments double-buffered by slice parity
   const int h = lane >> 5, r32 = lane & 31;
   bf16x8_t fa[2][Q], fb[2][Q];
-  auto read_frags = [&](int slot, int sl) {
+  // fragment r (0..2Q-1) of slice sl, in first-use order: a0 b0 .. b(Q-1) a1 .. a(Q-1)
+  auto read_frag = [&](int slot, int sl, int r) __attribute__((always_inline)) {
     const bf16_t* a = smem + slot * STAGE;
-#pragma unroll
-    for (int i = 0; i < Q; ++i) {
-      fa[sl & 1][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + swz(wm * WT + i * 32 + r32, 2 * sl + h)));
-      fb[sl & 1][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + A_ELTS + swz(wn * WT + i * 32 + r32, 2 * sl + h)));
-    }
+    if (r == 0)
+      fa[sl & 1][0] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + swz(wm * WT + r32, 2 * sl + h)));
+    else if (r <= Q)
+      fb[sl & 1][r - 1] =
+          __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + A_ELTS + swz(wn * WT + (r - 1) * 32 + r32, 2 * sl + h)));
+    else
+      fa[sl & 1][r - Q] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(a + swz(wm * WT + (r - Q) * 32 + r32, 2 * sl + h)));
   };
   f32x16_t acc[Q][Q];
 #pragma unroll
@@ -176,65 +208,56 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   // an (empty) AGPR operand makes the compiler select the AGPR form of the
   // MFMAs, which keeps the accumulators in place in the AGPR file
   asm volatile("" ::"a"(0.f));
-  auto mfma = [&](int sl, int q) {
+  auto mfma = [&](int sl, int q) __attribute__((always_inline)) {
     acc[q / Q][q % Q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[sl & 1][q / Q], fb[sl & 1][q % Q], acc[q / Q][q % Q], 0, 0, 0);
   };
 
   const int T = K / BK;
   // stage st; `full` = st + 2 < T (every condition below holds)
-  auto stage = [&](int st, bool full) {
+  auto stage = [&](int st, bool full) __attribute__((always_inline)) {
     const int slot = st & 1;
     const bool more = full || st + 1 < T;
     const bool dma_next = st > 0 && st + 1 < T;  // rest of stage st+1 (stage 1 comes whole with the prologue)
-    auto slice = [&](auto slc) {
+    const bool dma_far = full || st + 2 < T;     // first part of stage st+2
+    auto slice = [&](auto slc) __attribute__((always_inline)) {
       constexpr int sl = decltype(slc)::value;
-      constexpr int DN = sl == 0 ? D0 : sl == 1 ? D1 : 0;
-      constexpr int DB = D3 + (sl == 1 ? D0 : 0);
-      mfma(sl, 0);
-      mfma(sl, 1);
-      read_frags(slot, sl + 1);
-#pragma unroll
-      for (int q = 2; q < Q * Q; ++q) {
+      constexpr int DN = sl == 0 ? D0 : sl == 1 ? D1 : sl == 3 ? D3 : 0;
+      constexpr int DB = sl == 0 ? D3 : sl == 1 ? D3 + D0 : 0;
+      const int rslot = sl == 3 ? slot ^ 1 : slot;
+      const bool rd = sl < 3 || more;
+      const bool dd = sl == 3 ? dma_far : dma_next;
+      const int ds = sl == 3 ? st + 2 : st + 1;
+      static_for<0, Q * Q>([&](auto qc) __attribute__((always_inline)) {
+        constexpr int q = decltype(qc)::value;
         mfma(sl, q);
-        if (DN > 0 && q - 2 < DN && dma_next) dma(st + 1, DB + q - 2);
-      }
-      if (full) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);       // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * Q, 0);   // LDS read
-#pragma unroll
-        for (int k = 0; k < DN; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);     // VMEM read (DMA)
+        if constexpr (q < 2 * Q) {
+          if (rd) read_frag(rslot, (sl + 1) & 3, q);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, Q * Q - 2 - DN, 0);
+        if constexpr (q >= DMA_AT && (q - DMA_AT) % DMA_EVERY == 0 && (q - DMA_AT) / DMA_EVERY < DN) {
+          if (dd) dma(ds, DB + (q - DMA_AT) / DMA_EVERY);
+        }
+      });
+      if (full) {
+        static_for<0, Q * Q>([&](auto qc) __attribute__((always_inline)) {
+          constexpr int q = decltype(qc)::value;
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                    // MFMA
+          if constexpr (q < 2 * Q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+          if constexpr (q >= DMA_AT && (q - DMA_AT) % DMA_EVERY == 0 && (q - DMA_AT) / DMA_EVERY < DN)
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                  // VMEM read (DMA)
+        });
+      }
+      if constexpr (sl == 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (more) {
+          wait_vmcnt_lgkm0<0>();  // stage st+1 landed, this stage's reads returned
+          lds_barrier_pinned();
+        }
       }
     };
     slice(std::integral_constant<int, 0>{});
     slice(std::integral_constant<int, 1>{});
     slice(std::integral_constant<int, 2>{});
-    __builtin_amdgcn_sched_barrier(0);
-    if (more) {
-      wait_vmcnt_lgkm0<0>();  // stage st+1 landed, this stage's reads returned
-      lds_barrier_pinned();
-    }
-    mfma(3, 0);
-    mfma(3, 1);
-    if (more) read_frags(slot ^ 1, 0);
-#pragma unroll
-    for (int q = 2; q < Q * Q; ++q) {
-      mfma(3, q);
-      if (q - 2 < D3 && full) dma(st + 2, q - 2);
-    }
-    if (full) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * Q, 0);
-#pragma unroll
-      for (int k = 0; k < D3; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, Q * Q - 2 - D3, 0);
-    }
+    slice(std::integral_constant<int, 3>{});
   };
 
   // prologue: stages 0 and 1 whole, stage 0 landed everywhere, its first
@@ -249,7 +272,8 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
     wait_vmcnt_lgkm0<0>();
   }
   lds_barrier_pinned();
-  read_frags(0, 0);
+#pragma unroll
+  for (int r = 0; r < 2 * Q; ++r) read_frag(0, 0, r);
   int st = 0;
   for (; st + 2 < T; ++st) stage(st, true);
   for (; st < T; ++st) stage(st, false);
@@ -822,7 +846,7 @@ int gemm_check(int dtype, int epi, int M, int N, int K) {
   if (M < 0 || N <= 0 || K <= 0) return -1;
   if (epi == 2 && N % (2 * kGateUpBlock) != 0) return -1;
   if (dtype == 0) return 0;
-  if (dtype != 1 || K % 64 != 0) return -1;
+  if (dtype != 1 || K % 64 != 0 || K >= (1 << 21)) return -1;  // 32-bit byte offsets per 256-row tile
   if (M <= skinny::MAXM && N % 64 == 0) return 0;
   return (N % 256 == 0) ? 0 : -1;
 }

@@ -152,6 +152,16 @@ def test_device_calls_validate_before_touching_the_device():
     del ctypes
 
 
+def test_gemm_shapes_outside_the_kernels_are_rejected_on_the_host():
+    """K % 64, N % 256 (M > 64), the 32-bit offset bound K < 2^21 and the
+    SwiGLU pairing are checked before any launch (no GPU here)."""
+    buf = np.zeros(1 << 12, np.uint8)
+    p = buf.ctypes.data
+    for M, N, K, epi in [(256, 256, 100, 0), (256, 100, 64, 0), (256, 256, 1 << 21, 0), (32, 96, 64, 2)]:
+        rc = B.lib.ps_op_gemm(B.PS_BF16, 0, B.PS_BF16, epi, M, N, K, p, p, None, p, p, buf.nbytes, None)
+        assert rc == B.PS_E_UNSUPPORTED, (M, N, K, epi)
+
+
 def test_pack_gate_up_layout():
     F, d = 64, 3
     wg = np.arange(F * d, dtype=np.float32).reshape(F, d)
