@@ -43,19 +43,12 @@ template <> __device__ __forceinline__ void st_elt<float>(float* p, long i, floa
 template <> __device__ __forceinline__ void st_elt<bf16_t>(bf16_t* p, long i, float v) { p[i] = f2bf(v); }
 
 // ================================================================== helpers
-// One 16-byte global->LDS fill per lane (global_load_lds_dwordx4): a wave
-// instruction fills 1 KiB of LDS, lane l landing at +16 l. Kept in a
-// non-template device function: used directly inside a kernel template the
-// builtin makes the host pass drop the kernel's instantiation.
-__device__ __forceinline__ void load_lds16(const bf16_t* g, bf16_t* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-
-// The same fill through a buffer resource (buffer_load_dwordx4 ... lds):
-// `voffset` is the lane's byte offset from the resource base. The compiler
-// counts this form on vmcnt alone, so LDS reads issued around it keep exact
-// lgkmcnt waits; around the FLAT form above it waits for every outstanding
-// LDS read (lgkmcnt(0)) before each use of a fragment.
+// One 16-byte global->LDS fill per lane through a buffer resource
+// (buffer_load_dwordx4 ... lds): a wave instruction fills 1 KiB of LDS, lane
+// l landing at +16 l; `voffset` is the lane's byte offset from the resource
+// base. The compiler counts this form on vmcnt alone, so LDS reads issued
+// around it keep exact lgkmcnt waits (around the FLAT global_load_lds form
+// it waits for every outstanding LDS read before each use of a fragment).
 __device__ __forceinline__ void load_lds16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
 }
@@ -426,26 +419,30 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
   // chunk l%8, which holds global chunk (l%8) ^ (row%8)
   const int drow = lane >> 3, dch = (lane & 7) ^ (lane >> 3);
   const int n_ai = (TA - wave + 3) / 4;  // this wave's A instructions (0..2)
-  const bf16_t* asrc[2];
+  // DMA sources: buffer resources at the split's first activation column and
+  // at the workgroup's first W tile of the split, 32-bit lane byte offsets
+  const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(A + kb, (uint32_t)((long)(M - 1) * K + kps) * 2);
+  const __amdgpu_buffer_rsrc_t rW = buffer_rsrc(W + ((long)(n0 >> 6) * (K / 64) + kb / 64) * kWTileElts,
+                                                (uint32_t)((WN - 1) * (K / 64) + kps / 64) * kWTileElts * 2);
+  uint32_t aoff[2], woff[WI];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int row = (wave + 4 * i) * 8 + drow;
-    asrc[i] = A + (long)min(row, M - 1) * K + kb + dch * 8;
+    aoff[i] = ((uint32_t)min(row, M - 1) * K + dch * 8) * 2;
   }
   // tiled W: the stage's 64 k of each 64-row block is one contiguous tile
-  const bf16_t* wsrc[WI];
 #pragma unroll
   for (int i = 0; i < WI; ++i) {
-    const int n = n0 + (wave * WI + i) * 8 + drow;
-    wsrc[i] = W + ((long)(n >> 6) * (K / 64) + kb / 64) * kWTileElts + (n & 63) * 64 + dch * 8;
+    const int r = (wave * WI + i) * 8 + drow;  // row within the workgroup's WN blocks
+    woff[i] = ((uint32_t)(r >> 6) * (K / 64) * kWTileElts + (r & 63) * 64 + dch * 8) * 2;
   }
   auto dma = [&](int t, int slot) {
     bf16_t* st = smem + slot * STAGE;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      if (i < n_ai) load_lds16(asrc[i] + t * KS, st + (wave + 4 * i) * 8 * KS);
+      if (i < n_ai) load_lds16_buf(rA, aoff[i] + t * KS * 2, st + (wave + 4 * i) * 8 * KS);
 #pragma unroll
-    for (int i = 0; i < WI; ++i) load_lds16(wsrc[i] + (long)t * kWTileElts, st + AROWS * KS + (wave * WI + i) * 8 * KS);
+    for (int i = 0; i < WI; ++i) load_lds16_buf(rW, woff[i] + t * kWTileElts * 2, st + AROWS * KS + (wave * WI + i) * 8 * KS);
   };
   // this wave's own fills older than the most recent stage have landed
   auto wait_prev_stage = [&]() {
