@@ -21,7 +21,8 @@
 //
 // The pass is bound by the vector ALU (the softmax), not the matrix cores,
 // so the per-score vector work is kept minimal: the running max is taken on
-// raw scores and the scale folds into one FMA per exponent, and the row sum
+// raw scores and the scale folds into one FMA per exponent, the output is
+// rescaled only when a row's max outgrows the exponent base by 2^8, and the row sum
 // l comes from the matrix cores as a fifth O^T block whose A operand is all
 // ones (so l is the fp32 sum of exactly the bf16 P values the PV product
 // uses, and V == 1 gives exactly 1).
@@ -113,7 +114,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   const int voff = kPageTokens * kHd + (t >> 1) * kPageTokens + (t & 1) * 8;
   uint4 rk[2], rv[2];
   auto gload = [&](int k0) {
-    const bool full = k0 + kKT <= kv_valid;  // every key of the tile written
+    if (k0 + kKT <= kv_valid) {  // every key of the tile written: plain loads
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int pid = __builtin_amdgcn_readfirstlane(page_of((k0 + i * kPageTokens) / kPageTokens));
+        const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
+        rk[i] = *(const uint4*)(base + koff);
+        rv[i] = *(const uint4*)(base + voff);
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int p0 = k0 + i * kPageTokens;  // first position of page i
@@ -122,17 +132,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       if (p0 >= kv_valid) continue;
       const int pid = __builtin_amdgcn_readfirstlane(page_of(p0 / kPageTokens));
       const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
-      if (full || p0 + (t >> 4) < kv_valid) rk[i] = *(const uint4*)(base + koff);
+      if (p0 + (t >> 4) < kv_valid) rk[i] = *(const uint4*)(base + koff);
       uint4 w = *(const uint4*)(base + voff);
-      if (!full) {  // zero V^T entries of keys past the written length
-        const int valid = kv_valid - p0 - (t & 1) * 8;
-        if (valid < 8) {
-          uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+      // zero V^T entries of keys past the written length
+      const int valid = kv_valid - p0 - (t & 1) * 8;
+      if (valid < 8) {
+        uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (j >= valid) ws[j >> 1] &= (j & 1) ? 0x0000ffffu : 0xffff0000u;
-          w = make_uint4(ws[0], ws[1], ws[2], ws[3]);
-        }
+        for (int j = 0; j < 8; ++j)
+          if (j >= valid) ws[j >> 1] &= (j & 1) ? 0x0000ffffu : 0xffff0000u;
+        w = make_uint4(ws[0], ws[1], ws[2], ws[3]);
       }
       rv[i] = w;
     }
@@ -159,9 +168,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     const bf16_t* K = sK[buf];
     const bf16_t* V = sV[buf];
     // S^T for all row blocks, each K fragment read once
-    bool act[QB];
+    bool act[QB];  // block 0 always has a row (qn >= 1); a compile-time true keeps its products branch-free
 #pragma unroll
-    for (int cb = 0; cb < QB; ++cb) act[cb] = 32 * cb < qn;
+    for (int cb = 0; cb < QB; ++cb) act[cb] = cb == 0 || 32 * cb < qn;
     f32x16_t sacc[QB];
 #pragma unroll
     for (int cb = 0; cb < QB; ++cb)
@@ -192,21 +201,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
 #pragma unroll
       for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[cb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m[cb], mx);  // finite: key 0 is in tile 0
-      const float mb = m_new * scale_log2;
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i], scale_log2, -mb)),
-                             __builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i + 1], scale_log2, -mb)));
-      // rescale only if some row's running max moved (lane-local factor)
-      if (__any(m_new != m[cb])) {
-        const float alpha = __builtin_amdgcn_exp2f((m[cb] - m_new) * scale_log2);
+      // The exponent base m moves only when some row's max exceeds it by
+      // more than 8 in the exp2 domain (so P <= 2^8); O and l carry the
+      // same base, which cancels in O / l. Rows rarely cross the margin
+      // after the first tiles, so the 80-register rescale is mostly skipped.
+      // The first tile always moves it (m = -inf); key 0 is in every row's
+      // first tile, so m is finite from then on.
+      if (__any((mx - m[cb]) * scale_log2 > 8.f)) {
+        const float m_new = fmaxf(m[cb], mx);
+        const float alpha = __builtin_amdgcn_exp2f((m[cb] - m_new) * scale_log2);  // lane-local factor
 #pragma unroll
         for (int db = 0; db < 5; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[cb][db][r] *= alpha;
+        m[cb] = m_new;
       }
-      m[cb] = m_new;
+      const float mb = m[cb] * scale_log2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i], scale_log2, -mb)),
+                             __builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i + 1], scale_log2, -mb)));
     }
     // O^T += V^T P^T for all row blocks, each V fragment read once
 #pragma unroll
