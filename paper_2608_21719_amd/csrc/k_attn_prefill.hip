@@ -76,9 +76,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   // n_tiles 32-key tiles (the last tile may reach past the last query)
   const int n_tiles = (n_keys + kKT - 1) / kKT;
   const int n_pages_walk = min((kv_valid + kPageTokens - 1) / kPageTokens, n_tiles * (kKT / kPageTokens));
-  for (int i = t; i < min(n_pages_walk, kPageCache); i += NT) sPage[i] = btr[i];
+  // page ids of the walk, cached in LDS in windows of kPageCache pages
+  // (a tile's two pages never straddle a window: kPageCache is even)
+  int win = 0;  // first page of the cached window
+  auto fill_pages = [&]() {
+    for (int i = t; i < min(n_pages_walk - win, kPageCache); i += NT) sPage[i] = btr[win + i];
+  };
+  fill_pages();
   __syncthreads();
-  auto page_of = [&](int pg) { return pg < kPageCache ? sPage[pg] : btr[pg]; };
+  // page ids of the tile at key k0 (pages k0/16 and k0/16 + 1), one LDS read
+  auto tile_pages = [&](int k0) {
+    const int2 pp = *(const int2*)&sPage[k0 / kPageTokens - win];
+    return make_int2(__builtin_amdgcn_readfirstlane(pp.x), __builtin_amdgcn_readfirstlane(pp.y));
+  };
   const long kvh_off = (long)kvh * (2L * kPageTokens * kHd);
   const long page_stride = (long)n_kv * (2L * kPageTokens * kHd);
 
@@ -114,11 +124,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   const int voff = kPageTokens * kHd + (t >> 1) * kPageTokens + (t & 1) * 8;
   uint4 rk[2], rv[2];
   auto gload = [&](int k0) {
+    const int2 pids = tile_pages(k0);
     if (k0 + kKT <= kv_valid) {  // every key of the tile written: plain loads
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const int pid = __builtin_amdgcn_readfirstlane(page_of((k0 + i * kPageTokens) / kPageTokens));
-        const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
+        const bf16_t* base = pool + (long)(i ? pids.y : pids.x) * page_stride + kvh_off;
         rk[i] = *(const uint4*)(base + koff);
         rv[i] = *(const uint4*)(base + voff);
       }
@@ -130,7 +140,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       rk[i] = make_uint4(0, 0, 0, 0);
       rv[i] = make_uint4(0, 0, 0, 0);
       if (p0 >= kv_valid) continue;
-      const int pid = __builtin_amdgcn_readfirstlane(page_of(p0 / kPageTokens));
+      const int pid = i ? pids.y : pids.x;
       const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
       if (p0 + (t >> 4) < kv_valid) rk[i] = *(const uint4*)(base + koff);
       uint4 w = *(const uint4*)(base + voff);
@@ -164,7 +174,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   for (int kt = 0; kt < n_tiles; ++kt) {
     const int k0 = kt * kKT;
     const int buf = kt & 1;
-    if (kt + 1 < n_tiles) gload(k0 + kKT);
+    if (kt + 1 < n_tiles) {
+      if ((k0 + kKT) / kPageTokens - win >= kPageCache) {  // the next tile starts a new window
+        win += kPageCache;  // every wave is past its last read of the old window (barrier below)
+        fill_pages();
+        __syncthreads();
+      }
+      gload(k0 + kKT);
+    }
     const bf16_t* K = sK[buf];
     const bf16_t* V = sV[buf];
     // S^T for all row blocks, each K fragment read once

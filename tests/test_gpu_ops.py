@@ -390,6 +390,27 @@ def test_prefill_attention_ones_v_and_paging_invariance():
     assert np.all(H.to_f64(outs[(5, True)]) == 1.0)
 
 
+def test_prefill_attention_long_prefix_crosses_the_page_window():
+    """A 33-row chunk after a 33000-token prefix: the key walk spans more than
+    2048 pages (32768 positions), so the kernel's LDS cache of page ids moves
+    to its next window mid-walk; a short second sequence shares the launch."""
+    hist, new = [33000, 0], [33, 40]
+    P = make_pool(S8, 2100, 2, 2090, seed=21)
+    seqs, Ks, Vs = fill_kv(P, hist, new, "bf16", 700)
+    rows = sum(new)
+    q = rnd((rows, S8.n_q, S8.head_dim), "bf16", 63)
+    o = H.empty((rows, S8.d_q), "bf16")
+    B.op_attention(P.kv, 0, seqs, new, H.to_dev(q, "bf16"), o, H.workspace(1 << 22))
+    sync()
+    got = H.to_f64(o).reshape(rows, S8.n_q, S8.head_dim)
+    qf = gen.widen(q, "bf16")
+    r0 = 0
+    for b, (L, n) in enumerate(zip(hist, new)):
+        ref = O.attention(qf[r0:r0 + n], gen.widen(Ks[b], "bf16"), gen.widen(Vs[b], "bf16"), np.arange(L, L + n))
+        H.assert_close_elementwise(got[r0:r0 + n], ref, H.BF16_TOL_ABS, H.BF16_TOL_REL, f"long prefix b={b}")
+        r0 += n
+
+
 @pytest.mark.parametrize("hist,new", [([0, 3], [5, 1]), ([130, 0], [1, 40])])
 def test_attention_f32(hist, new):
     shape = TINY
