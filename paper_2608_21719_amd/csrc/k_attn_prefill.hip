@@ -3,8 +3,8 @@
 //
 // A workgroup owns one 64-row query tile of one sequence and one KV head;
 // its G waves are the G query heads of that group, so every K/V tile staged
-// in LDS serves all of them (GQA reuse). Keys are walked in 32-key tiles
-// (two pages) from position 0 up to the tile's last query position; the
+// in LDS serves all of them (GQA reuse). Keys are walked in 64-key tiles
+// (four pages) from position 0 up to the tile's last query position; the
 // cached prefix of a chunked prefill is just the first pages of the walk.
 //
 // Both products are arranged so that softmax statistics never cross lanes:
@@ -16,7 +16,7 @@
 // and O^T, so the online-softmax rescale is lane-local and the S^T
 // accumulator, exponentiated and rounded to bf16, is already the B operand
 // of the PV product. The V^T pages (dimension-major) make the A operand a
-// contiguous read. LDS rows are padded (272 B for K, 80 B for V^T) so the
+// contiguous read. LDS rows are padded (272 B for K, 144 B for V^T) so the
 // 16-byte operand reads of 16 consecutive lanes hit disjoint banks.
 //
 // The pass is bound by the vector ALU (the softmax), not the matrix cores,
@@ -33,9 +33,7 @@ namespace ps {
 
 namespace {
 constexpr int kHd = 128;
-constexpr int kKT = 32;              // keys per tile (two pages)
-constexpr int kKRow = kHd + 8;       // padded K row (elements)
-constexpr int kVRow = kKT + 8;       // padded V^T row (elements)
+constexpr int kFaKT = 64;            // keys per tile (four pages)
 constexpr int kPageCache = 2048;     // page ids cached in LDS (32768 positions)
 constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: lower register pressure, 2.3x faster than 2)
 }  // namespace
@@ -45,7 +43,7 @@ constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: low
 // next tile's global loads are issued into registers before the current
 // tile's products, and written to the other LDS buffer after them, so one
 // barrier per tile suffices and load latency hides behind the MFMAs.
-template <int QB>  // 32-row query blocks per wave; the workgroup's query tile is 32 * QB rows
+template <int QB, int KT>  // 32-row query blocks per wave (query tile 32 * QB rows); keys per tile
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
@@ -54,9 +52,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
                                                          bf16_t* __restrict__ o, int n_kv, int G, float scale_log2) {
   constexpr int NT = 256;
   constexpr int kQT = 32 * QB;
-  __shared__ __attribute__((aligned(16))) bf16_t sK[2][kKT * kKRow];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[2][kHd * kVRow];
-  __shared__ int32_t sPage[kPageCache];  // the walk's page ids (first kPageCache pages)
+  constexpr int NPG = KT / kPageTokens;  // pages per key tile
+  constexpr int NKB = KT / 32;           // 32-key blocks per key tile
+  constexpr int KRow = kHd + 8;          // padded K row (elements)
+  constexpr int VRow = KT + 8;           // padded V^T row (elements)
+  static_assert(KT % 32 == 0 && (NPG == 2 || NPG == 4) && kPageCache % NPG == 0, "key tile");
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][KT * KRow];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][kHd * VRow];
+  __shared__ __attribute__((aligned(16))) int32_t sPage[kPageCache];  // a window of the walk's page ids
 
   const int hq = G / 4;  // workgroups per KV head
   const int kvh = blockIdx.y / hq;
@@ -73,21 +76,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   const int kv_valid = s.kv_before + s.n_new;
   const int32_t* btr = bt + s.bt_off;
   // every page a tile load can touch: keys below kv_valid inside the walk's
-  // n_tiles 32-key tiles (the last tile may reach past the last query)
-  const int n_tiles = (n_keys + kKT - 1) / kKT;
-  const int n_pages_walk = min((kv_valid + kPageTokens - 1) / kPageTokens, n_tiles * (kKT / kPageTokens));
+  // n_tiles key tiles (the last tile may reach past the last query)
+  const int n_tiles = (n_keys + KT - 1) / KT;
+  const int n_pages_walk = min((kv_valid + kPageTokens - 1) / kPageTokens, n_tiles * NPG);
   // page ids of the walk, cached in LDS in windows of kPageCache pages
-  // (a tile's two pages never straddle a window: kPageCache is even)
+  // (a tile's pages never straddle a window: kPageCache is a multiple of NPG)
   int win = 0;  // first page of the cached window
   auto fill_pages = [&]() {
     for (int i = t; i < min(n_pages_walk - win, kPageCache); i += NT) sPage[i] = btr[win + i];
   };
   fill_pages();
   __syncthreads();
-  // page ids of the tile at key k0 (pages k0/16 and k0/16 + 1), one LDS read
-  auto tile_pages = [&](int k0) {
-    const int2 pp = *(const int2*)&sPage[k0 / kPageTokens - win];
-    return make_int2(__builtin_amdgcn_readfirstlane(pp.x), __builtin_amdgcn_readfirstlane(pp.y));
+  // page ids of the tile at key k0 (pages k0/16 ..), one LDS read
+  auto tile_pages = [&](int k0, int (&pid)[NPG]) {
+    const int* sp = &sPage[k0 / kPageTokens - win];
+    if constexpr (NPG == 4) {
+      const int4 pp = *(const int4*)sp;
+      pid[0] = __builtin_amdgcn_readfirstlane(pp.x);
+      pid[1] = __builtin_amdgcn_readfirstlane(pp.y);
+      pid[2] = __builtin_amdgcn_readfirstlane(pp.z);
+      pid[3] = __builtin_amdgcn_readfirstlane(pp.w);
+    } else {
+      const int2 pp = *(const int2*)sp;
+      pid[0] = __builtin_amdgcn_readfirstlane(pp.x);
+      pid[1] = __builtin_amdgcn_readfirstlane(pp.y);
+    }
   };
   const long kvh_off = (long)kvh * (2L * kPageTokens * kHd);
   const long page_stride = (long)n_kv * (2L * kPageTokens * kHd);
@@ -110,7 +123,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     for (int db = 0; db < 5; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[cb][db][r] = 0.f;
-  float m[QB];  // running max of raw (unscaled) scores
+  float m[QB];  // exponent base of each row block (raw, unscaled score units)
 #pragma unroll
   for (int cb = 0; cb < QB; ++cb) m[cb] = -INFINITY;
   bf16x8_t ones;
@@ -122,26 +135,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   // page ids are workgroup-uniform (scalar), the per-lane offsets fixed.
   const int koff = (t >> 4) * kHd + (t & 15) * 8;
   const int voff = kPageTokens * kHd + (t >> 1) * kPageTokens + (t & 1) * 8;
-  uint4 rk[2], rv[2];
+  uint4 rk[NPG], rv[NPG];
   auto gload = [&](int k0) {
-    const int2 pids = tile_pages(k0);
-    if (k0 + kKT <= kv_valid) {  // every key of the tile written: plain loads
+    int pids[NPG];
+    tile_pages(k0, pids);
+    if (k0 + KT <= kv_valid) {  // every key of the tile written: plain loads
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const bf16_t* base = pool + (long)(i ? pids.y : pids.x) * page_stride + kvh_off;
+      for (int i = 0; i < NPG; ++i) {
+        const bf16_t* base = pool + (long)pids[i] * page_stride + kvh_off;
         rk[i] = *(const uint4*)(base + koff);
         rv[i] = *(const uint4*)(base + voff);
       }
       return;
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NPG; ++i) {
       const int p0 = k0 + i * kPageTokens;  // first position of page i
       rk[i] = make_uint4(0, 0, 0, 0);
       rv[i] = make_uint4(0, 0, 0, 0);
       if (p0 >= kv_valid) continue;
-      const int pid = i ? pids.y : pids.x;
-      const bf16_t* base = pool + (long)pid * page_stride + kvh_off;
+      const bf16_t* base = pool + (long)pids[i] * page_stride + kvh_off;
       if (p0 + (t >> 4) < kv_valid) rk[i] = *(const uint4*)(base + koff);
       uint4 w = *(const uint4*)(base + voff);
       // zero V^T entries of keys past the written length
@@ -158,11 +171,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      *(uint4*)(&sK[buf][(16 * i + (t >> 4)) * kKRow + (t & 15) * 8]) = rk[i];
+    for (int i = 0; i < NPG; ++i) {
+      *(uint4*)(&sK[buf][(16 * i + (t >> 4)) * KRow + (t & 15) * 8]) = rk[i];
       // half hf = keys 8hf..8hf+7; stored per page as [0-3][8-11][4-7][12-15]
       const int dim = t >> 1, hf = t & 1;
-      bf16_t* dst = &sV[buf][dim * kVRow + i * kPageTokens];
+      bf16_t* dst = &sV[buf][dim * VRow + i * kPageTokens];
       *(uint2*)(dst + hf * 4) = make_uint2(rv[i].x, rv[i].y);
       *(uint2*)(dst + 8 + hf * 4) = make_uint2(rv[i].z, rv[i].w);
     }
@@ -172,51 +185,59 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   lstore(0);
   __syncthreads();
   for (int kt = 0; kt < n_tiles; ++kt) {
-    const int k0 = kt * kKT;
+    const int k0 = kt * KT;
     const int buf = kt & 1;
     if (kt + 1 < n_tiles) {
-      if ((k0 + kKT) / kPageTokens - win >= kPageCache) {  // the next tile starts a new window
+      if ((k0 + KT) / kPageTokens - win >= kPageCache) {  // the next tile starts a new window
         win += kPageCache;  // every wave is past its last read of the old window (barrier below)
         fill_pages();
         __syncthreads();
       }
-      gload(k0 + kKT);
+      gload(k0 + KT);
     }
     const bf16_t* K = sK[buf];
     const bf16_t* V = sV[buf];
-    // S^T for all row blocks, each K fragment read once
     bool act[QB];  // block 0 always has a row (qn >= 1); a compile-time true keeps its products branch-free
 #pragma unroll
     for (int cb = 0; cb < QB; ++cb) act[cb] = cb == 0 || 32 * cb < qn;
-    f32x16_t sacc[QB];
+    // S^T per 32-key block and row block, each K fragment read once
+    f32x16_t sacc[NKB][QB];
 #pragma unroll
-    for (int cb = 0; cb < QB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[cb][r] = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(K + c * kKRow + 16 * kk + 8 * g));
+    for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int cb = 0; cb < QB; ++cb)
-        if (act[cb]) sacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[cb][kk], sacc[cb], 0, 0, 0);
-    }
-    // sacc[cb][r] = score(key 8(r/4) + 4g + r%4, query 32cb + c); mask only
-    // on tiles that reach past the block's first query position
-    uint32_t pk[QB][8];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sacc[kb][cb][r] = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(K + (32 * kb + c) * KRow + 16 * kk + 8 * g));
+#pragma unroll
+        for (int cb = 0; cb < QB; ++cb)
+          if (act[cb]) sacc[kb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[cb][kk], sacc[kb][cb], 0, 0, 0);
+      }
+    // sacc[kb][cb][r] = score(key 32kb + 8(r/4) + 4g + r%4, query 32cb + c);
+    // mask only on tiles that reach past the block's first query position
+    uint32_t pk[NKB][QB][8];
 #pragma unroll
     for (int cb = 0; cb < QB; ++cb) {
       if (!act[cb]) continue;
       const int qpos = qpos0 + 32 * cb + c;
-      if (k0 + kKT - 1 > qpos0 + 32 * cb) {
+      if (k0 + KT - 1 > qpos0 + 32 * cb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key > qpos) sacc[cb][r] = -INFINITY;
-        }
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (key > qpos) sacc[kb][cb][r] = -INFINITY;
+          }
       }
-      float mx = sacc[cb][0];
+      float mx = sacc[0][cb][0];
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[cb][r]);
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][cb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       // The exponent base m moves only when some row's max exceeds it by
       // more than 8 in the exp2 domain (so P <= 2^8); O and l carry the
@@ -235,22 +256,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       }
       const float mb = m[cb] * scale_log2;
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        pk[cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i], scale_log2, -mb)),
-                             __builtin_amdgcn_exp2f(fmaf(sacc[cb][2 * i + 1], scale_log2, -mb)));
-    }
-    // O^T += V^T P^T for all row blocks, each V fragment read once
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-    for (int kk2 = 0; kk2 < 2; ++kk2) {
+        for (int i = 0; i < 8; ++i)
+          pk[kb][cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[kb][cb][2 * i], scale_log2, -mb)),
+                                   __builtin_amdgcn_exp2f(fmaf(sacc[kb][cb][2 * i + 1], scale_log2, -mb)));
+    }
+    // O^T += V^T P^T per page (16 keys) and row block, each V fragment read once
+#pragma unroll
+    for (int kk2 = 0; kk2 < NPG; ++kk2) {
+      const int kb = kk2 >> 1, hl = kk2 & 1;
       bf16x8_t bp[QB];
 #pragma unroll
       for (int cb = 0; cb < QB; ++cb)
-        bp[cb] = __builtin_bit_cast(
-            bf16x8_t, make_uint4(pk[cb][4 * kk2], pk[cb][4 * kk2 + 1], pk[cb][4 * kk2 + 2], pk[cb][4 * kk2 + 3]));
+        bp[cb] = __builtin_bit_cast(bf16x8_t, make_uint4(pk[kb][cb][4 * hl], pk[kb][cb][4 * hl + 1],
+                                                         pk[kb][cb][4 * hl + 2], pk[kb][cb][4 * hl + 3]));
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
         const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, *(const uint4*)(V + (32 * db + c) * kVRow + kk2 * kPageTokens + 8 * g));
+            bf16x8_t, *(const uint4*)(V + (32 * db + c) * VRow + kk2 * kPageTokens + 8 * g));
 #pragma unroll
         for (int cb = 0; cb < QB; ++cb)
           if (act[cb]) oacc[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp[cb], oacc[cb][db], 0, 0, 0);
@@ -290,7 +314,7 @@ int launch_fa_prefill_qb(int G, int n_items, int n_kv, const void* q, const void
   if (n_items == 0) return 0;
   if (G % 4 != 0) return -1;
   dim3 grid(n_items, n_kv * (G / 4));
-  hipLaunchKernelGGL(fa_prefill_kernel<QB>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si,
+  hipLaunchKernelGGL((fa_prefill_kernel<QB, kFaKT>), grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si,
                      bt, items, (bf16_t*)o, n_kv, G, scale_log2);
   return 0;
 }
