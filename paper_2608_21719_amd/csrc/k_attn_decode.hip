@@ -152,14 +152,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   const int end = it.page_end;
   int p = it.page_begin + wave;
   if (p < end) load_page(p, r0);
+  __builtin_amdgcn_sched_barrier(0);  // page p's loads first (the wait for it below counts on that order)
   if (p + 4 < end) load_page(p + 4, r1);
+  __builtin_amdgcn_sched_barrier(0);
+  // The scheduling barriers keep the order below: left free, the scheduler
+  // hoists the next page's score MFMAs above this page's, so every round
+  // began by waiting for both pages in flight (vmcnt(0)) and issued its
+  // next request only after that.
   for (; p + 16 < end; p += 12) {  // steady state: every request is a real page
     load_page(p + 8, r2);
+    __builtin_amdgcn_sched_barrier(0);
     page_compute(p, r0);
+    __builtin_amdgcn_sched_barrier(0);
     load_page(p + 12, r0);
+    __builtin_amdgcn_sched_barrier(0);
     page_compute(p + 4, r1);
+    __builtin_amdgcn_sched_barrier(0);
     load_page(p + 16, r1);
+    __builtin_amdgcn_sched_barrier(0);
     page_compute(p + 8, r2);
+    __builtin_amdgcn_sched_barrier(0);
   }
   if (p < end) {  // at most four pages left: p, p + 4, p + 8, p + 12
     if (p + 8 < end) load_page(p + 8, r2);
