@@ -362,6 +362,101 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   }
 }
 
+// Prefill-sized bf16 RoPE + KV write: 16 rows per workgroup (a page's worth
+// of tokens), the same arithmetic per element as rope_kvwrite_kernel. q and k
+// move eight pairs per thread with 16-byte accesses. v is staged through LDS:
+// when the 16 rows are one sequence's positions p0 .. p0+15 with p0 % 16 == 0
+// (they fill one page), each thread writes one dimension's 16 slots of the
+// dimension-major page as two 16-byte stores; otherwise 2-byte stores.
+constexpr int kRopeRows = 16;
+__global__ __launch_bounds__(256) void rope_kvwrite_rows_kernel(const bf16_t* __restrict__ qkv,
+                                                                bf16_t* __restrict__ q_out, bf16_t* __restrict__ pool,
+                                                                const SeqInfo* __restrict__ si,
+                                                                const int32_t* __restrict__ bt,
+                                                                const double* __restrict__ inv_freq, int rows,
+                                                                int n_seqs, int n_q, int n_kv, int hd) {
+  constexpr int RB = kRopeRows;
+  const int row0 = blockIdx.x * RB;
+  const int nr = min(RB, rows - row0);
+  const int half = hd >> 1;  // <= 64, a multiple of 8
+  const int dqkv = (n_q + 2 * n_kv) * hd;
+  const int vcols = n_kv * hd;
+  __shared__ float cs[RB][64], sn[RB][64];
+  __shared__ int s_b[RB], s_pos[RB], s_page[RB];
+  extern __shared__ __attribute__((aligned(16))) bf16_t sv[];  // [RB][vcols]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int r = wave; r < nr; r += 4) {
+    const int b = find_seq_wave(si, n_seqs, row0 + r);
+    if (lane == 0) {
+      const SeqInfo sq = si[b];
+      const int pos = sq.kv_before + (row0 + r - sq.row_start);
+      s_b[r] = b;
+      s_pos[r] = pos;
+      s_page[r] = bt[sq.bt_off + pos / kPageTokens];
+    }
+  }
+  // v rows of the block into LDS, 16 bytes per thread
+  const int vchunks = vcols / 8;
+  for (int idx = threadIdx.x; idx < nr * vchunks; idx += blockDim.x) {
+    const int r = idx / vchunks, ch = idx - r * vchunks;
+    *(uint4*)(sv + r * vcols + ch * 8) = *(const uint4*)(qkv + (long)(row0 + r) * dqkv + (n_q + n_kv) * hd + ch * 8);
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < nr * half; idx += blockDim.x) {
+    const int r = idx / half, j = idx - r * half;
+    double a = (double)s_pos[r] * inv_freq[j];
+    double sv_, cv;
+    sincos(a, &sv_, &cv);
+    cs[r][j] = (float)cv;
+    sn[r][j] = (float)sv_;
+  }
+  __syncthreads();
+  // q and k: pairs (j, j + half), eight consecutive j per thread
+  const int octs = half / 8;
+  const int per_row = (n_q + n_kv) * octs;
+  for (int idx = threadIdx.x; idx < nr * per_row; idx += blockDim.x) {
+    const int r = idx / per_row, rem = idx - r * per_row;
+    const int head = rem / octs, j = (rem - head * octs) * 8;
+    const bf16_t* xr = qkv + (long)(row0 + r) * dqkv + head * hd;
+    const uint4 a1 = *(const uint4*)(xr + j), a2 = *(const uint4*)(xr + j + half);
+    const uint32_t w1[4] = {a1.x, a1.y, a1.z, a1.w}, w2[4] = {a2.x, a2.y, a2.z, a2.w};
+    uint32_t o1[4], o2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x1l = bf_lo(w1[e]), x1h = bf_hi(w1[e]), x2l = bf_lo(w2[e]), x2h = bf_hi(w2[e]);
+      const float cl = cs[r][j + 2 * e], ch = cs[r][j + 2 * e + 1], sl = sn[r][j + 2 * e], sh = sn[r][j + 2 * e + 1];
+      o1[e] = pack_bf2(x1l * cl - x2l * sl, x1h * ch - x2h * sh);
+      o2[e] = pack_bf2(x2l * cl + x1l * sl, x2h * ch + x1h * sh);
+    }
+    bf16_t* d = head < n_q ? q_out + ((long)(row0 + r) * n_q + head) * hd
+                           : pool + kv_block(s_page[r], head - n_q, n_kv, hd) + (long)(s_pos[r] % kPageTokens) * hd;
+    *(uint4*)(d + j) = make_uint4(o1[0], o1[1], o1[2], o1[3]);
+    *(uint4*)(d + j + half) = make_uint4(o2[0], o2[1], o2[2], o2[3]);
+  }
+  // v: dimension-major within the page
+  const bool one_page = nr == RB && s_b[0] == s_b[RB - 1] && s_pos[0] % kPageTokens == 0;
+  if (one_page) {
+    for (int idx = threadIdx.x; idx < vcols; idx += blockDim.x) {
+      const int kvh = idx / hd, dim = idx - kvh * hd;
+      uint32_t w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        w[e] = (uint32_t)__builtin_bit_cast(uint16_t, sv[(2 * e) * vcols + idx]) |
+               ((uint32_t)__builtin_bit_cast(uint16_t, sv[(2 * e + 1) * vcols + idx]) << 16);
+      bf16_t* vb = pool + kv_block(s_page[0], kvh, n_kv, hd) + (long)kPageTokens * hd + (long)dim * kPageTokens;
+      *(uint4*)vb = make_uint4(w[0], w[1], w[2], w[3]);
+      *(uint4*)(vb + 8) = make_uint4(w[4], w[5], w[6], w[7]);
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < nr * vcols; idx += blockDim.x) {
+      const int r = idx / vcols, c = idx - r * vcols;
+      const int kvh = c / hd, dim = c - kvh * hd;
+      pool[kv_block(s_page[r], kvh, n_kv, hd) + (long)kPageTokens * hd + (long)dim * kPageTokens +
+           s_pos[r] % kPageTokens] = sv[r * vcols + c];
+    }
+  }
+}
+
 int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* pool_layer, const SeqInfo* si,
                         const int32_t* bt, const double* inv_freq, int n_seqs, int n_q, int n_kv, int hd,
                         hipStream_t st, const float* part, int splits) {
@@ -382,7 +477,15 @@ int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* po
 #undef ROPE_PART_CASE
     return -1;
   }
-  if (dt == 1)
+  const size_t v_lds = (size_t)kRopeRows * n_kv * hd * sizeof(bf16_t);
+  if (dt == 1 && hd % 16 == 0 && v_lds <= 64 * 1024) {
+    static const hipError_t attr = hipFuncSetAttribute((const void*)rope_kvwrite_rows_kernel,
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, 64 * 1024);
+    if (attr != hipSuccess) return -1;
+    hipLaunchKernelGGL(rope_kvwrite_rows_kernel, dim3((rows + kRopeRows - 1) / kRopeRows), dim3(256), v_lds, st,
+                       (const bf16_t*)qkv, (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, rows, n_seqs, n_q,
+                       n_kv, hd);
+  } else if (dt == 1)
     hipLaunchKernelGGL((rope_kvwrite_kernel<bf16_t, 0>), dim3(rows), dim3(256), 0, st, (const bf16_t*)qkv,
                        (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, n_seqs, n_q, n_kv, hd, nullptr, 0L);
   else

@@ -217,8 +217,11 @@ def test_kv_append_gather_bit_exact(dtype, shape):
 def test_rope_kvwrite(dtype, shape):
     P = H.Pool(shape, 128, 4, 64, seed=5)
     kv = P.kv
-    hist = [0, 5, 300]
-    new = [7, 16, 33]
+    # the last sequence starts at row 64 and position 32: rows 64..95 are two
+    # 16-row groups that each fill one page (the bf16 kernel's 16-byte V path);
+    # the other groups straddle sequences or pages (its 2-byte V path)
+    hist = [0, 5, 300, 32]
+    new = [7, 16, 41, 40]
     seqs = [kv.open() for _ in hist]
     ws = H.workspace(1 << 20)
     for s, L, n in zip(seqs, hist, new):
