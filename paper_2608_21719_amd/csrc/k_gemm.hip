@@ -399,7 +399,7 @@ constexpr size_t lds_bytes() { return (size_t)NS * (16 * MB + 64 * WN) * KS * 2;
 template <int MB, int WN, int EPI, typename TR, typename TC, bool DIRECT>
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                           float* __restrict__ part, const TR* __restrict__ R,
-                                                          TC* __restrict__ C, int M, int N, int K, int kps) {
+                                                          TC* __restrict__ C, int M, int N, int K, int S) {
   using namespace skinny;
   static_assert(!(DIRECT && EPI == 2) || WN == 2, "in-kernel SwiGLU pairs a gate and an up block per wave");
   static_assert(KS == kWTile, "one W tile per stage");
@@ -410,8 +410,12 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
   const int n0 = blockIdx.x * WROWS;
   const int split = blockIdx.y;
-  const int kb = split * kps;
-  const int T = kps / KS;
+  // split `split` of S takes 64-k stages [split TT / S, (split + 1) TT / S): near-equal ranges for any S
+  const int TT = K / KS;
+  const int st0 = split * TT / S;
+  const int T = (split + 1) * TT / S - st0;
+  const int kb = st0 * KS;
+  const int kps = T * KS;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
@@ -668,22 +672,24 @@ static int launch_reduce(int M, int N, int S, const float* part, const void* R, 
 // Skinny launch plan: WN 64-row blocks per workgroup and S K-splits. Two
 // blocks per workgroup halve the activation traffic per weight byte and win
 // whenever the grid still reaches ~160 workgroups; otherwise one block. The
-// split count doubles until the grid reaches its target, while each split
-// keeps at least 16 stages (shorter splits lose more to ring fill and
-// drain than they gain in parallelism, and add partial-sum traffic).
-// Chosen from a sweep of both widths and 1..8 splits over the 8B and 70B
-// decode shapes at M = 32 and 64, reduction included.
+// split count is the largest that keeps the grid within one round of 256
+// workgroups, at most 8, while each split keeps at least 16 stages (shorter
+// splits lose more to ring fill and drain than they gain in parallelism, and
+// add partial-sum traffic); splits are near-equal stage ranges, so any count
+// works. Chosen from a sweep of both widths and 1..8 splits over the 8B and
+// 70B decode shapes at M = 32 and 64, reduction included.
 static int skinny_splits_for(int tiles, int K, int target) {
   using namespace skinny;
-  int S = 1;
-  while (tiles * S < target && (K % (KS * S * 2)) == 0 && K / (S * 2) >= 16 * KS) S *= 2;
+  const int stages = K / KS;
+  int S = std::max(1, std::min(8, target / tiles));
+  while (S > 1 && stages / S < 16) --S;
   return S;
 }
 
 SkinnyPlan gemm_skinny_plan(int M, int N, int K) {
   (void)M;
   if (N % 128 == 0) {
-    const int S = skinny_splits_for(N / 128, K, 160);
+    const int S = skinny_splits_for(N / 128, K, 256);
     if ((N / 128) * S >= 160) return {2, S};
   }
   return {1, skinny_splits_for(N / 64, K, 256)};
@@ -697,7 +703,7 @@ static int launch_skinny_k(int M, int N, int K, int S, const void* A, const void
       (const void*)gemm_skinny_kernel<MB, WN, EPI, TR, TC, DIRECT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return -1;
   hipLaunchKernelGGL((gemm_skinny_kernel<MB, WN, EPI, TR, TC, DIRECT>), dim3(N / (64 * WN), S), dim3(skinny::NT), lds,
-                     st, (const bf16_t*)A, (const bf16_t*)W, part, (const TR*)R, (TC*)C, M, N, K, K / S);
+                     st, (const bf16_t*)A, (const bf16_t*)W, part, (const TR*)R, (TC*)C, M, N, K, S);
   return 0;
 }
 
@@ -721,7 +727,7 @@ static int launch_skinny_mb(int M, int N, int K, SkinnyPlan pl, const void* A, c
 template <int EPI, typename TR, typename TC>
 static int launch_skinny_plan(int M, int N, int K, SkinnyPlan pl, const void* A, const void* W, float* part,
                               const void* R, void* C, hipStream_t st) {
-  if ((pl.wn != 1 && pl.wn != 2) || N % (64 * pl.wn) != 0 || pl.s < 1 || K % (skinny::KS * pl.s) != 0) return -1;
+  if ((pl.wn != 1 && pl.wn != 2) || N % (64 * pl.wn) != 0 || pl.s < 1 || K / skinny::KS < pl.s) return -1;
   switch ((M + 15) / 16) {
     case 1: return launch_skinny_mb<1, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
     case 2: return launch_skinny_mb<2, EPI, TR, TC>(M, N, K, pl, A, W, part, R, C, st);
@@ -805,7 +811,7 @@ int launch_gemm(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, con
 }
 
 // launch_gemm, except that a decode-sized bf16 GEMM whose plan splits K in
-// 2, 4 or 8 stops at the split partials (fp32 [S][M][N] at the head of ws,
+// 2, 3, 4 or 8 stops at the split partials (fp32 [S][M][N] at the head of ws,
 // summed in split order by the consumer, which fuses the reduction with its
 // own work); *splits = S then, else 1 and C holds the result.
 int launch_gemm_split(int dtype, int r_dt, int c_dt, int epi, int M, int N, int K, const void* A, const void* W,
@@ -813,7 +819,7 @@ int launch_gemm_split(int dtype, int r_dt, int c_dt, int epi, int M, int N, int 
   *splits = 1;
   if (dtype == 1 && M > 0 && M <= skinny::MAXM && N % 64 == 0 && K % 64 == 0 && epi != 2) {
     const SkinnyPlan pl = gemm_skinny_plan(M, N, K);
-    if (pl.s == 2 || pl.s == 4 || pl.s == 8) {  // the split counts the fused consumers take
+    if (pl.s == 2 || pl.s == 3 || pl.s == 4 || pl.s == 8) {  // the split counts the fused consumers take
       if (ws_bytes < gemm_workspace_bytes(dtype, M, N, K)) return -2;
       *splits = pl.s;
       float* part = (float*)ws;

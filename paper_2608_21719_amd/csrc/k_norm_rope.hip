@@ -165,6 +165,7 @@ int launch_split_residual_rmsnorm(int rows, int d, int S, const float* part, con
     return 0;                                                                                               \
   }
   SRR_CASE(2)
+  SRR_CASE(3)
   SRR_CASE(4)
   SRR_CASE(8)
 #undef SRR_CASE
@@ -472,6 +473,7 @@ int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* po
       return 0;                                                                                                 \
     }
     ROPE_PART_CASE(2)
+    ROPE_PART_CASE(3)
     ROPE_PART_CASE(4)
     ROPE_PART_CASE(8)
 #undef ROPE_PART_CASE
