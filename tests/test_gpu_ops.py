@@ -64,7 +64,11 @@ def gemm_bound(a, w, K, out_bf16):
 
 @pytest.mark.parametrize("M,N,K", [(300, 512, 448), (256, 256, 64), (520, 768, 1024),   # tile path
                                    (64, 256, 1024), (37, 192, 512), (1, 64, 256), (17, 320, 2048),  # skinny
-                                   (64, 32768, 256), (33, 16384, 2048)])  # skinny, two blocks per workgroup
+                                   (64, 32768, 256), (33, 16384, 2048),  # skinny, two blocks per workgroup
+                                   # skinny with 3, 5, 6, 7 K splits (one block) and 3 (two blocks); each K is a
+                                   # stage count the split count does not divide, so the last split is longer
+                                   (24, 4480, 3136), (64, 2880, 5184), (8, 2560, 6208), (50, 2304, 7232),
+                                   (40, 10240, 3136)])
 def test_gemm_store_bf16(M, N, K):
     a = rnd((M, K), "bf16", 3)
     w = rnd((N, K), "bf16", 4, 0.02)
@@ -81,7 +85,7 @@ def test_gemm_store_bf16(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 512, 448), (64, 256, 1024), (5, 128, 256), (64, 256, 4096), (64, 16384, 2048),
-                                   (40, 20480, 128)])
+                                   (40, 20480, 128), (64, 2880, 5184)])
 @pytest.mark.parametrize("rdt,cdt", [("bf16", "f32"), ("f32", "bf16")])
 def test_gemm_residual(M, N, K, rdt, cdt):
     a = rnd((M, K), "bf16", 5)
