@@ -52,6 +52,11 @@ template <> __device__ __forceinline__ void st_elt<bf16_t>(bf16_t* p, long i, fl
 __device__ __forceinline__ void load_lds16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
 }
+// The same with the non-temporal hint (cache policy bit 1), for data read
+// exactly once per call (decode weight streams).
+__device__ __forceinline__ void load_lds16_buf_nt(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 2);
+}
 // Raw (stride 0) buffer resource over `bytes` bytes from `base`; loads past
 // the end return zero.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
@@ -446,7 +451,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const bf16_t* __restri
     for (int i = 0; i < 2; ++i)
       if (i < n_ai) load_lds16_buf(rA, aoff[i] + t * KS * 2, st + (wave + 4 * i) * 8 * KS);
 #pragma unroll
-    for (int i = 0; i < WI; ++i) load_lds16_buf(rW, woff[i] + t * kWTileElts * 2, st + AROWS * KS + (wave * WI + i) * 8 * KS);
+    for (int i = 0; i < WI; ++i) load_lds16_buf_nt(rW, woff[i] + t * kWTileElts * 2, st + AROWS * KS + (wave * WI + i) * 8 * KS);
   };
   // this wave's own fills older than the most recent stage have landed
   auto wait_prev_stage = [&]() {
