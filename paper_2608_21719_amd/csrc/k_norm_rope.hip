@@ -363,14 +363,15 @@ __global__ __launch_bounds__(256) void rope_kvwrite_kernel(const T* __restrict__
   }
 }
 
-// Prefill-sized bf16 RoPE + KV write: 16 rows per workgroup (a page's worth
-// of tokens), the same arithmetic per element as rope_kvwrite_kernel. q and k
+// Prefill-sized bf16 RoPE + KV write: 16 rows per workgroup of 1024 threads
+// (a page's worth of tokens; about one sequence lookup per wave and one angle
+// per thread), the same arithmetic per element as rope_kvwrite_kernel. q and k
 // move eight pairs per thread with 16-byte accesses. v is staged through LDS:
 // when the 16 rows are one sequence's positions p0 .. p0+15 with p0 % 16 == 0
 // (they fill one page), each thread writes one dimension's 16 slots of the
 // dimension-major page as two 16-byte stores; otherwise 2-byte stores.
 constexpr int kRopeRows = 16;
-__global__ __launch_bounds__(256) void rope_kvwrite_rows_kernel(const bf16_t* __restrict__ qkv,
+__global__ __launch_bounds__(1024) void rope_kvwrite_rows_kernel(const bf16_t* __restrict__ qkv,
                                                                 bf16_t* __restrict__ q_out, bf16_t* __restrict__ pool,
                                                                 const SeqInfo* __restrict__ si,
                                                                 const int32_t* __restrict__ bt,
@@ -385,8 +386,8 @@ __global__ __launch_bounds__(256) void rope_kvwrite_rows_kernel(const bf16_t* __
   __shared__ float cs[RB][64], sn[RB][64];
   __shared__ int s_b[RB], s_pos[RB], s_page[RB];
   extern __shared__ __attribute__((aligned(16))) bf16_t sv[];  // [RB][vcols]
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int r = wave; r < nr; r += 4) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, n_waves = blockDim.x >> 6;
+  for (int r = wave; r < nr; r += n_waves) {
     const int b = find_seq_wave(si, n_seqs, row0 + r);
     if (lane == 0) {
       const SeqInfo sq = si[b];
@@ -484,7 +485,7 @@ int launch_rope_kvwrite(int dt, int rows, const void* qkv, void* q_out, void* po
     static const hipError_t attr = hipFuncSetAttribute((const void*)rope_kvwrite_rows_kernel,
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, 64 * 1024);
     if (attr != hipSuccess) return -1;
-    hipLaunchKernelGGL(rope_kvwrite_rows_kernel, dim3((rows + kRopeRows - 1) / kRopeRows), dim3(256), v_lds, st,
+    hipLaunchKernelGGL(rope_kvwrite_rows_kernel, dim3((rows + kRopeRows - 1) / kRopeRows), dim3(1024), v_lds, st,
                        (const bf16_t*)qkv, (bf16_t*)q_out, (bf16_t*)pool_layer, si, bt, inv_freq, rows, n_seqs, n_q,
                        n_kv, hd);
   } else if (dt == 1)
