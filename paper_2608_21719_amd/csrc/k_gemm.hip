@@ -370,10 +370,12 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
       if (row >= M) continue;
       const long idx = (long)row * ldc + ccol + oc;
       if constexpr (std::is_same<TC, bf16_t>::value) {
-        *(uint4*)(C + idx) = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
-                                        pack_bf2(v[6], v[7]));
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        __builtin_nontemporal_store(u32x4{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
+                                          pack_bf2(v[6], v[7])}, (u32x4*)(C + idx));
       } else {
-        *(float4*)(C + idx) = make_float4(v[0], v[1], v[2], v[3]);
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, (f32x4*)(C + idx));
       }
     }
   }
