@@ -29,18 +29,37 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const bf16_t* __restri
   for (int e = threadIdx.x * 8; e < d; e += 256 * 8) *(uint4*)(dst + i * d + e) = *(const uint4*)(src + r * d + e);
 }
 
-// next[r] = argmax_j logits[r, j], ties to the lowest j. One workgroup per row.
-__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int32_t* __restrict__ next,
-                                                     int vocab) {
+// next[r] = argmax_j logits[r, j], ties to the lowest j. One workgroup of
+// 1024 threads per row, 16-byte loads where the row allows (a decode step has
+// only as many rows as sequences, so each row needs many loads in flight).
+// NaN never compares greater; an all-NaN row gives 0.
+constexpr int kArgmaxThreads = 1024;
+__global__ __launch_bounds__(kArgmaxThreads) void argmax_kernel(const float* __restrict__ logits,
+                                                                int32_t* __restrict__ next, int vocab) {
   const long r = blockIdx.x;
   const float* row = logits + r * vocab;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int j = threadIdx.x; j < vocab; j += 256) {
-    const float v = row[j];
-    if (v > best) {  // strictly greater: j increases, so ties keep the lowest index
-      best = v;
-      bi = j;
+  // each thread visits its indices in increasing order, and "strictly
+  // greater" then keeps the lowest index among equal values
+  if (vocab % 4 == 0 && ((uintptr_t)row & 15) == 0) {
+    const int n4 = vocab / 4;
+#pragma unroll 4
+    for (int j4 = threadIdx.x; j4 < n4; j4 += kArgmaxThreads) {
+      const float4 v = *(const float4*)(row + 4 * (long)j4);
+      const int j = 4 * j4;
+      if (v.x > best) { best = v.x; bi = j; }
+      if (v.y > best) { best = v.y; bi = j + 1; }
+      if (v.z > best) { best = v.z; bi = j + 2; }
+      if (v.w > best) { best = v.w; bi = j + 3; }
+    }
+  } else {
+    for (int j = threadIdx.x; j < vocab; j += kArgmaxThreads) {
+      const float v = row[j];
+      if (v > best) {
+        best = v;
+        bi = j;
+      }
     }
   }
   for (int off = 32; off > 0; off >>= 1) {
@@ -51,20 +70,20 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ l
       bi = oi;
     }
   }
-  __shared__ float sv[4];
-  __shared__ int si_[4];
+  constexpr int NW = kArgmaxThreads / 64;
+  __shared__ float sv[NW];
+  __shared__ int si_[NW];
   if ((threadIdx.x & 63) == 0) {
     sv[threadIdx.x >> 6] = best;
     si_[threadIdx.x >> 6] = bi;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < NW; ++w)
       if (sv[w] > best || (sv[w] == best && si_[w] < bi)) {
         best = sv[w];
         bi = si_[w];
       }
-    // an all-NaN row keeps index 0x7fffffff: clamp to 0 so callers get a valid id
     next[r] = bi == 0x7fffffff ? 0 : bi;
   }
 }
@@ -133,7 +152,7 @@ int launch_gather_rows(int n, int d, const void* src, const int32_t* rows, void*
 
 int launch_argmax(int rows, int vocab, const float* logits, int32_t* next, hipStream_t st) {
   if (rows == 0) return 0;
-  hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(256), 0, st, logits, next, vocab);
+  hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(kArgmaxThreads), 0, st, logits, next, vocab);
   return 0;
 }
 

@@ -35,8 +35,9 @@ def accept_tokens(got_tok, ref_logits, what):
         assert ref_logits[i][t] >= mx - tau, f"{what} row {i}: token {t} logit {ref_logits[i][t]:.4f} < max {mx:.4f} - {tau:.3f}"
 
 
-def test_argmax_full_vocab_with_ties():
-    rows, vocab = 64, 128256
+@pytest.mark.parametrize("vocab", [128256, 1001])  # 16-byte loads; an odd vocabulary takes 4-byte loads
+def test_argmax_full_vocab_with_ties(vocab):
+    rows = 64
     r = np.random.default_rng(1)
     lg = r.standard_normal((rows, vocab)).astype(np.float32)
     for i in range(rows):  # plant a tie between two maxima
