@@ -31,8 +31,12 @@
  *    pointers are borrowed for the duration of the call.
  *  - Work is enqueued asynchronously on the caller's stream (a hipStream_t
  *    passed as void*; NULL = the null stream). Nothing synchronises
- *    implicitly, except that reuse of a staging slot waits for the upload
- *    that last used it (a small kernel reading the pinned slot).
+ *    implicitly, except that reuse of a staging slot waits on the host for
+ *    the upload that last used it (a small kernel reading the pinned slot,
+ *    which then stores a done tag into pinned host memory; the wait fails
+ *    with PS_E_HIP after 60 s). Destroying a KV handle waits up to 10 s for
+ *    its outstanding uploads, and leaves the ring allocated if they have not
+ *    run by then.
  *  - Device buffers (activations, weights, KV pool, workspace) must be
  *    16-byte aligned: kernels move them with 16-byte vector accesses.
  *    Unaligned pointers are rejected with PS_E_INVALID.

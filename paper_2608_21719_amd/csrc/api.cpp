@@ -4,11 +4,14 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstring>
 #include <initializer_list>
 #include <new>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/ps.h"
@@ -65,34 +68,59 @@ ps_status check_cfg(const ps_layer_cfg* c) {
 }
 
 // Pinned host staging ring for per-call metadata. A slot is reused only
-// after the copy that last read it has completed.
+// after the upload kernel that last read it has run: every workgroup of that
+// kernel stores the upload's tag into a word of pinned host memory once its
+// reads are done, and the host waits for those words (no event sits in the
+// caller's stream, so nothing there depends on which streams the calls use).
 struct Staging {
   static constexpr int kSlots = 4;
   void* host[kSlots] = {};
   void* mapped[kSlots] = {};  // device-side address of host[s]
   size_t cap[kSlots] = {};
-  hipEvent_t ev[kSlots] = {};
-  bool pending[kSlots] = {};
+  uint32_t* done = nullptr;  // kSlots x kUploadMaxBlocks words written by the upload kernel
+  uint32_t* done_mapped = nullptr;
+  uint32_t tag[kSlots] = {};  // tag of the slot's last upload
+  int blocks[kSlots] = {};    // its workgroups; 0 = nothing outstanding
+  uint32_t last_tag = 0;
   int next = 0;
 
+  // Waits until slot s's last upload has read the slot; false after
+  // `limit` with the upload still outstanding.
+  bool wait(int s, std::chrono::seconds limit) {
+    if (!blocks[s]) return true;
+    const volatile uint32_t* d = done + (size_t)s * kUploadMaxBlocks;
+    const auto t0 = std::chrono::steady_clock::now();
+    for (int b = 0; b < blocks[s]; ++b)
+      for (unsigned spin = 0; d[b] != tag[s]; ++spin) {
+        std::this_thread::yield();
+        if ((spin & 4095) == 4095 && std::chrono::steady_clock::now() - t0 > limit) return false;
+      }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    blocks[s] = 0;
+    return true;
+  }
   ~Staging() {
-    for (int s = 0; s < kSlots; ++s) {
-      if (pending[s]) (void)hipEventSynchronize(ev[s]);
-      if (ev[s]) (void)hipEventDestroy(ev[s]);
+    bool drained = true;
+    for (int s = 0; s < kSlots; ++s) drained = wait(s, std::chrono::seconds(10)) && drained;
+    if (!drained) return;  // the device may still read the ring: leave it allocated
+    for (int s = 0; s < kSlots; ++s)
       if (host[s]) (void)hipHostFree(host[s]);
-    }
+    if (done) (void)hipHostFree(done);
   }
   // Returns the slot index or -1 (g_err set).
   int acquire(size_t bytes, void** out) {
-    const int s = next;
-    next = (next + 1) % kSlots;
     hipError_t e;
-    if (pending[s]) {
-      if ((e = hipEventSynchronize(ev[s])) != hipSuccess) return (hip_fail(e, "staging wait"), -1);
-      pending[s] = false;
+    if (!done) {
+      const size_t nb = sizeof(uint32_t) * kSlots * kUploadMaxBlocks;
+      if ((e = hipHostMalloc((void**)&done, nb, hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
+        return (done = nullptr, hip_fail(e, "staging hipHostMalloc"), -1);
+      std::memset(done, 0, nb);
+      if ((e = hipHostGetDevicePointer((void**)&done_mapped, done, 0)) != hipSuccess)
+        return (hip_fail(e, "staging device pointer"), -1);
     }
-    if (!ev[s] && (e = hipEventCreateWithFlags(&ev[s], hipEventDisableTiming)) != hipSuccess)
-      return (hip_fail(e, "staging event"), -1);
+    const int s = next;
+    if (!wait(s, std::chrono::seconds(60)))
+      return (fail(PS_E_HIP, "staging wait: the upload that last used the slot has not run after 60 s"), -1);
     if (cap[s] < bytes) {
       if (host[s]) (void)hipHostFree(host[s]);
       host[s] = mapped[s] = nullptr;
@@ -111,13 +139,18 @@ struct Staging {
   }
   // Copies the slot's first `bytes`, rounded up to 16, to `dev` on `st`
   // (slots are acquired for the 256-aligned metadata size, and the
-  // destination always has that much room).
+  // destination always has that much room). The ring advances only here, so
+  // a slot acquired by a call that then failed is simply acquired again.
   ps_status submit(int s, void* dev, size_t bytes, hipStream_t st) {
-    if (launch_upload(mapped[s], dev, align_up(bytes, 16), st)) return fail(PS_E_INVALID, "metadata upload size");
+    const uint32_t t = last_tag + 1 ? last_tag + 1 : 1;  // 0 is the words' initial value
+    const int nb = launch_upload(mapped[s], dev, align_up(bytes, 16), done_mapped + (size_t)s * kUploadMaxBlocks, t, st);
+    if (nb < 0) return fail(PS_E_INVALID, "metadata upload size");
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "metadata upload");
-    if ((e = hipEventRecord(ev[s], st)) != hipSuccess) return hip_fail(e, "staging event record");
-    pending[s] = true;
+    last_tag = t;
+    tag[s] = t;
+    blocks[s] = nb;
+    next = (s + 1) % kSlots;
     return PS_OK;
   }
 };

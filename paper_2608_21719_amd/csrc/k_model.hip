@@ -91,19 +91,28 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_kernel(const float* __r
 // dst[i] = src[i] for n 16-byte units; src is pinned host memory mapped into
 // the device address space (the per-call metadata upload, done by a kernel
 // rather than a DMA-engine copy because the copy's start-up latency would
-// otherwise sit between the previous call's last kernel and this call's first)
+// otherwise sit between the previous call's last kernel and this call's first).
+// Each workgroup then stores `tag` into done[blockIdx.x], a word of pinned
+// host memory: every load of src has returned by then (each loaded value was
+// stored to dst before the barrier), so once all of the grid's words read
+// `tag` the host may overwrite src. The host learns this without an event in
+// the stream, whose marker would hold the next kernel back.
 __global__ __launch_bounds__(256) void upload16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                                       long n) {
+                                                       long n, uint32_t* __restrict__ done, uint32_t tag) {
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) dst[i] = src[i];
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(done + blockIdx.x, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, hipStream_t st) {
+int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag,
+                  hipStream_t st) {
   if (bytes == 0) return 0;
   if (bytes % 16) return -1;
   const long n = (long)(bytes / 16);
-  const int blocks = (int)std::min<long>((n + 255) / 256, 64);
-  hipLaunchKernelGGL(upload16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)host_dev_ptr, (uint4*)dst, n);
-  return 0;
+  const int blocks = (int)std::min<long>((n + 255) / 256, kUploadMaxBlocks);
+  hipLaunchKernelGGL(upload16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)host_dev_ptr, (uint4*)dst, n,
+                     done, tag);
+  return blocks;
 }
 
 // Row-major W[N, K] -> 64x64 tiles (layout in common.h): one thread per

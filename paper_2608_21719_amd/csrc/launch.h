@@ -50,7 +50,11 @@ SkinnyPlan gemm_skinny_plan(int M, int N, int K);
 int gemm_check(int dtype, int epi, int M, int N, int K);
 
 // model-level kernels (bf16 rows)
-int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, hipStream_t st);
+// Copies `bytes` (a multiple of 16) from mapped host memory to dst, then each
+// workgroup stores `tag` to done[workgroup]. Returns the number of workgroups
+// (0 for no bytes, at most kUploadMaxBlocks) or -1 for a bad size.
+constexpr int kUploadMaxBlocks = 64;
+int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag, hipStream_t st);
 int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st);
 int launch_gather_rows(int n, int d, const void* src, const int32_t* rows, void* dst, hipStream_t st);
 int launch_argmax(int rows, int vocab, const float* logits, int32_t* next, hipStream_t st);
