@@ -122,20 +122,30 @@ struct Staging {
     if (!wait(s, std::chrono::seconds(60)))
       return (fail(PS_E_HIP, "staging wait: the upload that last used the slot has not run after 60 s"), -1);
     if (cap[s] < bytes) {
-      if (host[s]) (void)hipHostFree(host[s]);
-      host[s] = mapped[s] = nullptr;
-      cap[s] = 0;
-      const size_t nb = align_up(std::max<size_t>(bytes, 1 << 16), 1 << 16);
-      // coherent (uncached on the device): the upload kernel reads what the
-      // host wrote just before the launch
-      if ((e = hipHostMalloc(&host[s], nb, hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
-        return (hip_fail(e, "staging hipHostMalloc"), -1);
-      if ((e = hipHostGetDevicePointer(&mapped[s], host[s], 0)) != hipSuccess)
-        return (hip_fail(e, "staging device pointer"), -1);
-      cap[s] = nb;
+      if (!grow(s, bytes)) return -1;
+      // slots never used yet are allocated now too, so that a loop of calls
+      // does not pay a pinned allocation in each of its first kSlots calls
+      for (int j = 0; j < kSlots; ++j)
+        if (!host[j] && !grow(j, bytes)) return -1;
     }
     *out = host[s];
     return s;
+  }
+  // (Re)allocates slot j, which no outstanding upload reads, for `bytes`.
+  bool grow(int j, size_t bytes) {
+    if (host[j]) (void)hipHostFree(host[j]);
+    host[j] = mapped[j] = nullptr;
+    cap[j] = 0;
+    const size_t nb = align_up(std::max<size_t>(bytes, 1 << 16), 1 << 16);
+    hipError_t e;
+    // coherent (uncached on the device): the upload kernel reads what the
+    // host wrote just before the launch
+    if ((e = hipHostMalloc(&host[j], nb, hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
+      return (host[j] = nullptr, hip_fail(e, "staging hipHostMalloc"), false);
+    if ((e = hipHostGetDevicePointer(&mapped[j], host[j], 0)) != hipSuccess)
+      return (hip_fail(e, "staging device pointer"), false);
+    cap[j] = nb;
+    return true;
   }
   // Copies the slot's first `bytes`, rounded up to 16, to `dev` on `st`
   // (slots are acquired for the 256-aligned metadata size, and the

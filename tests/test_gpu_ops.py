@@ -216,6 +216,42 @@ def test_kv_append_gather_bit_exact(dtype, shape):
         np.testing.assert_array_equal(hv, vb)
 
 
+def test_metadata_slots_reused_while_the_gpu_lags_on_two_streams():
+    """Per-call metadata goes through a 4-slot pinned ring. Here the host runs far ahead of a busy GPU and
+    alternates two streams, so every slot is rewritten many times while earlier uploads may still wait in
+    a queue; each gather must still see its own sequence (length, block table)."""
+    shape = S8
+    P = H.Pool(shape, 256, 12, 64, seed=5)
+    kv = P.kv
+    lens = [1, 15, 16, 17, 33, 64, 100, 161, 250, 333]
+    seqs = [kv.open() for _ in lens]
+    ws0 = H.workspace(1 << 20)
+    ks, vs = [], []
+    for i, (s, L) in enumerate(zip(seqs, lens)):
+        kv.alloc(s, L)
+        k, v = rnd((L, shape.n_kv, shape.head_dim), "bf16", 60 + i), rnd((L, shape.n_kv, shape.head_dim), "bf16", 80 + i)
+        kv.append(0, [s], [L], H.to_dev(k, "bf16"), H.to_dev(v, "bf16"), ws0)
+        kv.commit([s], [L])
+        ks.append(k)
+        vs.append(v)
+    calls = [(r, i) for r in range(3) for i in range(len(lens))]
+    outs = [(H.empty((lens[i], shape.n_kv, shape.head_dim), "bf16"),
+             H.empty((lens[i], shape.n_kv, shape.head_dim), "bf16"), H.workspace(1 << 16)) for _, i in calls]
+    busy = torch.randn(6144, 6144, device="cuda")
+    sync()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for st in streams:
+        with torch.cuda.stream(st):
+            for _ in range(2):
+                busy @ busy  # keeps the queue busy while the host enqueues every gather
+    for c, ((_, i), (ko, vo, ws)) in enumerate(zip(calls, outs)):
+        kv.gather(0, seqs[i], ko, vo, ws, stream=streams[c % 2])
+    sync()
+    for (_, i), (ko, vo, _) in zip(calls, outs):
+        np.testing.assert_array_equal(H.bits(ko), ks[i].view(np.int16))
+        np.testing.assert_array_equal(H.bits(vo), vs[i].view(np.int16))
+
+
 # ------------------------------------------------------------------ RoPE
 @pytest.mark.parametrize("dtype,shape", [("bf16", S8), ("f32", TINY)])
 def test_rope_kvwrite(dtype, shape):
