@@ -147,21 +147,29 @@ struct Staging {
     cap[j] = nb;
     return true;
   }
-  // Copies the slot's first `bytes`, rounded up to 16, to `dev` on `st`
+  // The upload of the slot's first `bytes`, rounded up to 16, to `dev`
   // (slots are acquired for the 256-aligned metadata size, and the
-  // destination always has that much room). The ring advances only here, so
-  // a slot acquired by a call that then failed is simply acquired again.
-  ps_status submit(int s, void* dev, size_t bytes, hipStream_t st) {
+  // destination always has that much room). Marks the slot as read by that
+  // upload: the caller enqueues the job (launch_upload, or a kernel that
+  // carries it) before it touches the ring again. The ring advances only
+  // here, so a slot acquired by a call that then failed is acquired again.
+  ps_status prepare(int s, void* dev, size_t bytes, UploadJob* job) {
     const uint32_t t = last_tag + 1 ? last_tag + 1 : 1;  // 0 is the words' initial value
-    const int nb = launch_upload(mapped[s], dev, align_up(bytes, 16), done_mapped + (size_t)s * kUploadMaxBlocks, t, st);
-    if (nb < 0) return fail(PS_E_INVALID, "metadata upload size");
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "metadata upload");
+    if (!make_upload_job(mapped[s], dev, align_up(bytes, 16), done_mapped + (size_t)s * kUploadMaxBlocks, t, job))
+      return fail(PS_E_INVALID, "metadata upload size");
     last_tag = t;
     tag[s] = t;
-    blocks[s] = nb;
+    blocks[s] = job->blocks;
     next = (s + 1) % kSlots;
     return PS_OK;
+  }
+  // prepare + the upload as its own kernel on `st`.
+  ps_status submit(int s, void* dev, size_t bytes, hipStream_t st) {
+    UploadJob j;
+    if (ps_status rc = prepare(s, dev, bytes, &j)) return rc;
+    launch_upload(j, st);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PS_OK : hip_fail(e, "metadata upload");
   }
 };
 
@@ -700,9 +708,21 @@ ps_status upload_meta(ps_kv* kv, const Meta& mt, void* ws, hipStream_t st) {
   return kv->staging.submit(slot, ws, mt.buf.size(), st);
 }
 
+// upload_meta, except that the upload is returned as a job for the caller's
+// first kernel to carry (which must then be enqueued).
+ps_status stage_meta(ps_kv* kv, const Meta& mt, void* ws, UploadJob* job) {
+  void* host;
+  const int slot = kv->staging.acquire(mt.size(), &host);
+  if (slot < 0) return PS_E_HIP;
+  std::memcpy(host, mt.buf.data(), mt.buf.size());
+  return kv->staging.prepare(slot, ws, mt.buf.size(), job);
+}
+
 // The kernels of one layer: x_in -> x_out for the planned rows.
+// `up`, if given, is the call's metadata upload: the first kernel carries it
+// (every kernel that reads the metadata runs after that one).
 int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w, void* pool, const void* x_in,
-                 void* x_out, char* W, hipStream_t st) {
+                 void* x_out, char* W, hipStream_t st, const UploadJob* up = nullptr) {
   const WsLayout& wl = P.wl;
   const int d = c.hidden, dq = c.n_q_heads * c.head_dim, dkv = c.n_kv_heads * c.head_dim;
   const int dt = c.dtype, G = group_of(c), rows = P.rows;
@@ -720,7 +740,7 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
   const float scale = 1.0f / std::sqrt((float)c.head_dim);
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
   int bad = 0;
-  bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st);
+  bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st, up);
   // decode-sized QKV: RoPE + KV write sums the split-K partials itself
   // (bf16, head_dim a multiple of 8: the fused reader's vector width)
   int s_qkv = 1;
@@ -797,8 +817,9 @@ ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, 
   P.wl = layout(c, P.mt.size(), P.rows, P.n_parts);
   if (ps_status rc = check_ws(ws, ws_bytes, P.wl.total)) return rc;
   hipStream_t st = (hipStream_t)stream;
-  if (ps_status rc = upload_meta(kv, P.mt, ws, st)) return rc;
-  if (launch_layer(c, P, w, kv->layer_base(layer), x_in, x_out, (char*)ws, st))
+  UploadJob up;
+  if (ps_status rc = stage_meta(kv, P.mt, ws, &up)) return rc;
+  if (launch_layer(c, P, w, kv->layer_base(layer), x_in, x_out, (char*)ws, st, &up))
     return fail(PS_E_UNSUPPORTED, "a kernel rejected its configuration");
   return last_launch_error();
 }

@@ -88,31 +88,24 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_kernel(const float* __r
   }
 }
 
-// dst[i] = src[i] for n 16-byte units; src is pinned host memory mapped into
-// the device address space (the per-call metadata upload, done by a kernel
-// rather than a DMA-engine copy because the copy's start-up latency would
-// otherwise sit between the previous call's last kernel and this call's first).
-// Each workgroup then stores `tag` into done[blockIdx.x], a word of pinned
-// host memory: every load of src has returned by then (each loaded value was
-// stored to dst before the barrier), so once all of the grid's words read
-// `tag` the host may overwrite src. The host learns this without an event in
-// the stream, whose marker would hold the next kernel back.
-__global__ __launch_bounds__(256) void upload16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                                       long n, uint32_t* __restrict__ done, uint32_t tag) {
-  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) dst[i] = src[i];
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(done + blockIdx.x, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+__global__ __launch_bounds__(256) void upload16_kernel(UploadJob j) { upload_block(j, blockIdx.x); }
+
+bool make_upload_job(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag, UploadJob* j) {
+  if (bytes % 16) return false;
+  *j = UploadJob{};
+  j->src = host_dev_ptr;
+  j->dst = dst;
+  j->n16 = (long)(bytes / 16);
+  j->done = done;
+  j->tag = tag;
+  j->blocks = (int)std::min<long>((j->n16 + 255) / 256, kUploadMaxBlocks);
+  return true;
 }
 
-int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag,
-                  hipStream_t st) {
-  if (bytes == 0) return 0;
-  if (bytes % 16) return -1;
-  const long n = (long)(bytes / 16);
-  const int blocks = (int)std::min<long>((n + 255) / 256, kUploadMaxBlocks);
-  hipLaunchKernelGGL(upload16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)host_dev_ptr, (uint4*)dst, n,
-                     done, tag);
-  return blocks;
+int launch_upload(const UploadJob& j, hipStream_t st) {
+  if (j.blocks == 0) return 0;
+  hipLaunchKernelGGL(upload16_kernel, dim3(j.blocks), dim3(256), 0, st, j);
+  return 0;
 }
 
 // Row-major W[N, K] -> 64x64 tiles (layout in common.h): one thread per

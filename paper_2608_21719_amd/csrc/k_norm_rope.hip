@@ -71,10 +71,16 @@ __device__ __forceinline__ void rmsnorm_row_out(const float (&v)[VPT][8], const 
 
 // Vectorised bf16 -> bf16 variant: 8 elements per 16-byte access, the row
 // kept in registers between the two passes (d <= 256 * 8 * VPT).
+// The first up.blocks workgroups carry a metadata upload instead (the first
+// kernel of a layer call takes its call's upload along, saving a launch).
 template <typename TX, int VPT>
 __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const TX* __restrict__ x, const bf16_t* __restrict__ g,
-                                                          bf16_t* __restrict__ y, int d, float eps) {
-  const long row = blockIdx.x;
+                                                          bf16_t* __restrict__ y, int d, float eps, UploadJob up) {
+  if ((int)blockIdx.x < up.blocks) {
+    upload_block(up, blockIdx.x);
+    return;
+  }
+  const long row = blockIdx.x - up.blocks;
   float v[VPT][8];
 #pragma unroll
   for (int c = 0; c < VPT; ++c) {
@@ -172,20 +178,29 @@ int launch_split_residual_rmsnorm(int rows, int d, int S, const float* part, con
   return -1;
 }
 
+bool rmsnorm_carries_upload(int x_dt, int g_dt, int y_dt, int d) {
+  (void)x_dt;
+  return g_dt == 1 && y_dt == 1 && d % 8 == 0 && d <= 256 * 8 * 4;
+}
+
 int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
-                   void* y, hipStream_t st) {
-  if (rows == 0) return 0;
-  dim3 grid(rows), block(256);
-  if (g_dt == 1 && y_dt == 1 && d % 8 == 0 && d <= 256 * 8 * 4) {
+                   void* y, hipStream_t st, const UploadJob* up) {
+  if (rmsnorm_carries_upload(x_dt, g_dt, y_dt, d)) {
+    const UploadJob j = up ? *up : UploadJob{};
+    if (rows + j.blocks == 0) return 0;
+    dim3 grid(rows + j.blocks), block(256);
     if (x_dt == 1) {
       hipLaunchKernelGGL((rmsnorm_vec_kernel<bf16_t, 4>), grid, block, 0, st, (const bf16_t*)x,
-                         (const bf16_t*)g, (bf16_t*)y, d, eps);
+                         (const bf16_t*)g, (bf16_t*)y, d, eps, j);
     } else {
       hipLaunchKernelGGL((rmsnorm_vec_kernel<float, 4>), grid, block, 0, st, (const float*)x,
-                         (const bf16_t*)g, (bf16_t*)y, d, eps);
+                         (const bf16_t*)g, (bf16_t*)y, d, eps, j);
     }
     return 0;
   }
+  if (up && launch_upload(*up, st)) return -1;
+  if (rows == 0) return 0;
+  dim3 grid(rows), block(256);
 #define RMS_CASE(TX_, TG_, TY_, a, b, c)                                                           \
   if (x_dt == a && g_dt == b && y_dt == c) {                                                       \
     hipLaunchKernelGGL((rmsnorm_kernel<TX_, TG_, TY_>), grid, block, 0, st, (const TX_*)x,        \

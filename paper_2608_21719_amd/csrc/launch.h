@@ -10,8 +10,9 @@
 namespace ps {
 
 // dtype codes: 0 = fp32, 1 = bf16
+struct UploadJob;
 int launch_rmsnorm(int x_dt, int g_dt, int y_dt, int rows, int d, const void* x, const void* g, float eps,
-                   void* y, hipStream_t st);
+                   void* y, hipStream_t st, const UploadJob* up = nullptr);
 
 // part/splits: when splits > 1 (bf16), the QKV rows are the sum of `splits`
 // fp32 split-K partials at part (see launch_gemm_split), qkv is not read
@@ -50,11 +51,38 @@ SkinnyPlan gemm_skinny_plan(int M, int N, int K);
 int gemm_check(int dtype, int epi, int M, int N, int K);
 
 // model-level kernels (bf16 rows)
-// Copies `bytes` (a multiple of 16) from mapped host memory to dst, then each
-// workgroup stores `tag` to done[workgroup]. Returns the number of workgroups
-// (0 for no bytes, at most kUploadMaxBlocks) or -1 for a bad size.
+// One metadata upload: n16 16-byte units from mapped host memory (src) to
+// dst, then each of its `blocks` workgroups stores `tag` to done[workgroup].
 constexpr int kUploadMaxBlocks = 64;
-int launch_upload(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag, hipStream_t st);
+struct UploadJob {
+  const void* src = nullptr;
+  void* dst = nullptr;
+  long n16 = 0;
+  uint32_t* done = nullptr;
+  uint32_t tag = 0;
+  int blocks = 0;  // 0: nothing to copy
+};
+// Workgroup b of the job (256 threads): copies its share, then stores the
+// tag. Every load of src has returned before the tag store (each loaded value
+// was stored to dst before the barrier), so once all `blocks` words read the
+// tag the host may overwrite src. The host learns this without an event in
+// the stream, whose marker would hold the next kernel back. The copy is done
+// by a kernel, not a DMA-engine copy, whose start-up latency would sit
+// between the previous call's last kernel and this call's first.
+__device__ inline void upload_block(const UploadJob& j, int b) {
+  const uint4* src = (const uint4*)j.src;
+  uint4* dst = (uint4*)j.dst;
+  for (long i = (long)b * 256 + threadIdx.x; i < j.n16; i += (long)j.blocks * 256) dst[i] = src[i];
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(j.done + b, j.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+// Fills the job for `bytes` (a multiple of 16); false for a bad size.
+bool make_upload_job(const void* host_dev_ptr, void* dst, size_t bytes, uint32_t* done, uint32_t tag, UploadJob* j);
+// Enqueues the job as its own kernel.
+int launch_upload(const UploadJob& j, hipStream_t st);
+// True when launch_rmsnorm for these types runs the kernel that can carry an
+// upload job in leading workgroups of its own grid.
+bool rmsnorm_carries_upload(int x_dt, int g_dt, int y_dt, int d);
 int launch_embed(int rows, int d, int vocab, const void* table, const int32_t* tokens, void* x, hipStream_t st);
 int launch_gather_rows(int n, int d, const void* src, const int32_t* rows, void* dst, hipStream_t st);
 int launch_argmax(int rows, int vocab, const float* logits, int32_t* next, hipStream_t st);
