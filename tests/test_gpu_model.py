@@ -147,6 +147,57 @@ def test_small_model_prefill_then_decode():
         accept_tokens(nxt.cpu().numpy(), ref_logits, f"decode {step}")
 
 
+def test_small_model_decode_equals_single_layer_calls_bit_for_bit():
+    """The model call (embedding, the layer stack in one call, final norm, LM head, argmax) and the same decode
+    step through single-layer calls and the head ops give the same bits: logits, next tokens and every KV byte
+    written. The model call shares one metadata upload across its layers; the layer calls each upload their
+    own."""
+    wl, layers, head = small_model_parts()
+    sh, L, V = wl.shape, wl.n_layers, wl.vocab
+    dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
+    dev_head = {k: (H.to_dev_w if k == "lm_head" else H.to_dev)(v, "bf16") for k, v in head.items()}
+    pools = [H.Pool(sh, 64, 4, 8, n_layers=L, seed=21) for _ in range(2)]
+    model = B.Model(pools[0].cfg, [d.w for d in dev_layers], V, dev_head["embed"], dev_head["final_norm"],
+                    dev_head["lm_head"])
+    lens = [40, 23]
+    ws = H.workspace(B.Model.workspace_bytes(pools[0].cfg, V, 128, 4, 8))
+    dtok = torch.from_numpy(gen.token_ids(wl, sum(lens))).cuda()
+    nxt = torch.empty(len(lens), dtype=torch.int32, device="cuda")
+    seqs = []
+    for P in pools:
+        ss = [P.kv.open() for _ in lens]
+        for s, n in zip(ss, lens):
+            P.kv.alloc(s, n + 4)
+        model.prefill(P.kv, ss, lens, dtok, nxt, ws)
+        P.kv.commit(ss, lens)
+        seqs.append(ss)
+    sync()
+    t = torch.from_numpy(gen.token_ids(wl, len(lens), step=1)).cuda()
+    logits_m = torch.empty((len(lens), V), dtype=torch.float32, device="cuda")
+    nxt_m = torch.empty(len(lens), dtype=torch.int32, device="cuda")
+    model.decode_step(pools[0].kv, B.PS_PHASE_ANSWER, seqs[0], t, nxt_m, ws, logits_m)
+
+    layer = B.Layer(pools[1].cfg)
+    lws = H.workspace(B.Layer.workspace_bytes(pools[1].cfg, 64, 4, 8))
+    x = dev_head["embed"][t.long()].contiguous()
+    for l in range(L):
+        y = torch.empty_like(x)
+        layer.decode_step(dev_layers[l].w, pools[1].kv, l, B.PS_PHASE_ANSWER, seqs[1], x, y, lws)
+        x = y
+    hn = torch.empty_like(x)
+    B.op_rmsnorm(B.PS_BF16, B.PS_BF16, B.PS_BF16, len(lens), sh.hidden, x, dev_head["final_norm"], sh.eps, hn)
+    logits_c = torch.empty((len(lens), V), dtype=torch.float32, device="cuda")
+    gws = H.workspace(max(16, B.op_gemm_workspace_bytes(B.PS_BF16, len(lens), V, sh.hidden)))
+    B.op_gemm(B.PS_BF16, 0, B.PS_F32, B.PS_EPI_STORE, len(lens), V, sh.hidden, hn, dev_head["lm_head"], None,
+              logits_c, gws)
+    nxt_c = torch.empty(len(lens), dtype=torch.int32, device="cuda")
+    B.op_argmax(len(lens), V, logits_c, nxt_c)
+    sync()
+    assert torch.equal(logits_m.view(torch.int32), logits_c.view(torch.int32))
+    assert torch.equal(nxt_m, nxt_c)
+    assert torch.equal(pools[0].mem.view(torch.uint8), pools[1].mem.view(torch.uint8))
+
+
 def test_model_rejects_shallow_pool():
     wl, layers, head = small_model_parts(n_layers=2, vocab=256)
     dev_layers = [H.DeviceLayer(w, "bf16") for w in layers]
