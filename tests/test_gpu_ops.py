@@ -2,7 +2,7 @@
 
 Each stage is teacher-forced: the oracle evaluates the stage on exactly the
 bf16 / fp32 values the device received, so the bound is the stage's own
-rounding (SURVEY reading: |g - r| <= 2e-2 + 1e-2 |r| for bf16 outputs),
+rounding (|g - r| <= 2e-2 + 1e-2 |r| for bf16 outputs: a few bf16 ulps of the result),
 except where a tighter deterministic bound exists (GEMM, bit-exact paging).
 """
 import numpy as np
