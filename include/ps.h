@@ -149,12 +149,18 @@ ps_status ps_op_tile_weight(int32_t dtype, int32_t N, int32_t K, const void* w, 
 size_t ps_kv_pool_bytes(const ps_layer_cfg* cfg, int32_t n_layers, int32_t n_pages);
 
 /* Host-only: creates the metadata. `pool` is borrowed until destroy and not
- * touched by this call. */
+ * touched by this call. A pool is the KV capacity of one instance: §III-C
+ * (Observation 3) bounds decode concurrency by the bytes each token pins
+ * (320 KiB per token for a 70B-class model), and §IV-A gives each stage pool
+ * (prefill / think / answer) its own. */
 ps_status ps_kv_create(const ps_layer_cfg* cfg, int32_t n_layers, int32_t n_pages, int32_t max_seqs,
                        int32_t max_pages_per_seq, void* pool, uint64_t page_order_seed, ps_kv** out);
 ps_status ps_kv_destroy(ps_kv* kv);
 
-/* Host-only metadata calls. */
+/* Host-only metadata calls. ps_kv_alloc is the per-request, per-stage KV
+ * reservation in tokens (the "KV chunk size" CS_i of §III-B's design-space
+ * table and §IV-A: CS_T for think, CS_A for answer); PS_E_NO_PAGES when the
+ * free pages cannot cover it, with nothing reserved. */
 ps_status ps_kv_seq_open(ps_kv* kv, int32_t* seq);                 /* new empty sequence id        */
 ps_status ps_kv_alloc(ps_kv* kv, int32_t seq, int32_t n_tokens);   /* reserve: capacity >= len + n */
 ps_status ps_kv_commit(ps_kv* kv, int32_t n_seqs, const int32_t* seqs, const int32_t* n_tok);
@@ -171,12 +177,16 @@ ps_status ps_kv_block_table(const ps_kv* kv, int32_t seq, int32_t* pages, int32_
 /* Device calls. `ws` is caller-provided device workspace of ws_bytes bytes
  * (at least ps_workspace_bytes for the call's size).
  *
- * ps_kv_append: write caller K and V rows (already rotated keys) for `layer`
- * at positions [len, len + n_tok[i]) of each sequence; k, v are
- * [sum n_tok, n_kv, hd] device arrays, rows grouped by sequence in order.
- * Does not change len (see ps_kv_commit).
- * ps_kv_gather: copy positions [0, len) of one sequence and layer into
- * contiguous k_out, v_out [len, n_kv, hd] (export, tests). */
+ * ps_kv_append (§II-B decode: every generated token's keys and values join
+ * the cache that later steps read): write caller K and V rows (already
+ * rotated keys) for `layer` at positions [len, len + n_tok[i]) of each
+ * sequence; k, v are [sum n_tok, n_kv, hd] device arrays, rows grouped by
+ * sequence in order. Does not change len (see ps_kv_commit). Errors: capacity
+ * not reserved (PS_E_CAPACITY), bad layer or sequence (PS_E_INVALID).
+ * ps_kv_gather (§V "What does KV transfer cost": the think -> answer handoff
+ * moves a sequence's KV state out of one pool): copy positions [0, len) of
+ * one sequence and layer into contiguous k_out, v_out [len, n_kv, hd]. Both
+ * are bit-exact copies through the block table. */
 ps_status ps_kv_append(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
                        const int32_t* n_tok, const void* k, const void* v, void* ws, size_t ws_bytes,
                        void* stream);
@@ -192,7 +202,9 @@ ps_status ps_layer_destroy(ps_layer* layer);
 size_t ps_workspace_bytes(const ps_layer_cfg* cfg, int32_t max_rows, int32_t max_seqs,
                           int32_t max_pages_per_seq);
 
-/* Prefill (or a chunk of one): each sequence i contributes n_tok[i] rows of
+/* Prefill (§II-B: attention over every prompt token at once, compute-bound;
+ * App. B.2 eq. flops-layer counts its work) or a chunk of one: each
+ * sequence i contributes n_tok[i] rows of
  * x_in [sum n_tok, d] at positions [len_i, len_i + n_tok[i]); its K/V for
  * `layer` are written there (capacity must be reserved) and every row
  * attends causally over positions 0..pos (cached prefix included). x_out
@@ -201,13 +213,19 @@ ps_status ps_prefill(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer,
                      const int32_t* seqs, const int32_t* n_tok, const void* x_in, void* x_out, void* ws,
                      size_t ws_bytes, void* stream);
 
-/* Decode: one new row per sequence at position len (its K/V appended before
- * attention, so it attends over len + 1 keys). x_in, x_out [n_seqs, d]. */
+/* Decode (§II-B: one token per sequence per step, bound by reading the KV
+ * cache; §III-C: the think phase is the same step over far longer contexts;
+ * App. B.2 eqs. bytes-layer and gamma): one new row per sequence at position
+ * len (its K/V appended before attention, so it attends over len + 1 keys).
+ * x_in, x_out [n_seqs, d]. `phase` is PS_PHASE_THINK or PS_PHASE_ANSWER (the
+ * §IV-A stage tag); it may change scheduling only, never the result. */
 ps_status ps_decode_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t phase,
                          int32_t n_seqs, const int32_t* seqs, const void* x_in, void* x_out, void* ws,
                          size_t ws_bytes, void* stream);
 
-/* Mixed step (chunked prefill fused with decode): the GEMMs run once over
+/* Mixed step (chunked prefill fused with decode; §II-B's phases served by one
+ * batch, as the serving systems the paper builds on do when new requests
+ * join a running decode batch): the GEMMs run once over
  * the concatenated rows — first the chunk rows of n_chunk sequences
  * (chunk_tok[i] rows each), then one row for each of n_dec decoding
  * sequences; attention uses the prefill path for chunk rows and the split-K

@@ -147,6 +147,36 @@ def layer_sequence(w: dict, shape, x: np.ndarray, k_hist: np.ndarray = None,
             "pos": pos}
 
 
+def layer_rows(w: dict, shape, x: np.ndarray, rows, k_hist: np.ndarray = None,
+               v_hist: np.ndarray = None) -> np.ndarray:
+    """The same layer as layer_sequence, output of the selected new rows only.
+
+    Keys and values come from every row (attention needs them); the query,
+    attention, projections and FFN are evaluated for `rows` (indices into x)
+    alone. Rows are independent except through attention, so each result
+    equals the matching row of layer_sequence. Returns out [len(rows), d].
+    """
+    n, d = x.shape
+    nq, nkv, hd = shape.n_q, shape.n_kv, shape.head_dim
+    if k_hist is None:
+        k_hist = np.zeros((0, nkv, hd))
+        v_hist = np.zeros((0, nkv, hd))
+    L = k_hist.shape[0]
+    pos = np.arange(L, L + n)
+    rows = np.asarray(rows)
+    xn = rmsnorm(x, w["attn_norm"], shape.eps)
+    k_new = rope(linear(xn, w["wk"]).reshape(n, nkv, hd), pos, shape.theta)
+    v_new = linear(xn, w["wv"]).reshape(n, nkv, hd)
+    K = np.concatenate([k_hist, k_new], axis=0)
+    V = np.concatenate([v_hist, v_new], axis=0)
+    q = rope(linear(xn[rows], w["wq"]).reshape(len(rows), nq, hd), pos[rows], shape.theta)
+    o = attention(q, K, V, pos[rows]).reshape(len(rows), nq * hd)
+    h = x[rows] + linear(o, w["wo"])
+    hn = rmsnorm(h, w["ffn_norm"], shape.eps)
+    m = silu(linear(hn, w["wg"])) * linear(hn, w["wu"])
+    return h + linear(m, w["wd"])
+
+
 def layer_batch(w: dict, shape, xs, hists=None) -> list:
     """The layer over several independent sequences (no cross-sequence attention)."""
     res = []

@@ -55,6 +55,14 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 int elt_bytes(int dt) { return dt == PS_BF16 ? 2 : 4; }
 
+// Field by field: ps_layer_cfg has tail padding after `dtype`, which a
+// caller's separately built configurations need not agree on.
+bool same_cfg(const ps_layer_cfg& a, const ps_layer_cfg& b) {
+  return a.hidden == b.hidden && a.n_q_heads == b.n_q_heads && a.n_kv_heads == b.n_kv_heads &&
+         a.head_dim == b.head_dim && a.ffn == b.ffn && a.rms_eps == b.rms_eps && a.rope_theta == b.rope_theta &&
+         a.dtype == b.dtype;
+}
+
 ps_status check_cfg(const ps_layer_cfg* c) {
   if (!c) return fail(PS_E_INVALID, "null config");
   if (c->dtype != PS_F32 && c->dtype != PS_BF16) return fail(PS_E_INVALID, "dtype must be PS_F32 or PS_BF16");
@@ -806,7 +814,7 @@ ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, 
   CHECK_KV(kv);
   if (ps_status rc = check_weights(w)) return rc;
   const ps_layer_cfg& c = L->cfg;
-  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0)
+  if (!same_cfg(c, kv->cfg))
     return fail(PS_E_INVALID, "layer and KV pool configurations differ");
   if (ps_status rc = check_layer(kv, layer)) return rc;
   LayerPlan P;
@@ -857,7 +865,7 @@ ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, cons
   if (!M) return fail(PS_E_INVALID, "null model handle");
   CHECK_KV(kv);
   const ps_layer_cfg& c = M->cfg;
-  if (std::memcmp(&c, &kv->cfg, sizeof(c)) != 0) return fail(PS_E_INVALID, "model and KV pool configurations differ");
+  if (!same_cfg(c, kv->cfg)) return fail(PS_E_INVALID, "model and KV pool configurations differ");
   if (kv->n_layers < M->n_layers) return fail(PS_E_INVALID, "KV pool has fewer layers than the model");
   LayerPlan P;
   if (ps_status rc = plan_layer(c, kv, phase, n_chunk, chunk_seqs, chunk_tok, n_dec, dec_seqs, P)) return rc;

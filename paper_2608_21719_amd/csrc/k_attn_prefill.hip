@@ -1,8 +1,9 @@
 // Prefill (and chunked-prefill) causal attention over the paged KV cache,
 // bf16 in, fp32 softmax, on the gfx950 matrix cores.
 //
-// A workgroup owns one 64-row query tile of one sequence and one KV head;
-// its G waves are the G query heads of that group, so every K/V tile staged
+// A workgroup owns one 32-row query tile (32 * kFaQB rows, kFaQB = 1) of one
+// sequence and one KV head; its waves are four query heads of that group
+// (two workgroups per KV head when G = 8), so every K/V tile staged
 // in LDS serves all of them (GQA reuse). Keys are walked in 64-key tiles
 // (four pages) from position 0 up to the tile's last query position; the
 // cached prefix of a chunked prefill is just the first pages of the walk.

@@ -71,6 +71,19 @@ def normal(shape, std: float, dtype: str, cfg_id: int, layer: int, code: int, st
 
 
 # ---------------------------------------------------------------- weights
+def _draw(specs: dict) -> dict:
+    """normal() for each named spec, the tensors drawn in parallel threads.
+
+    Each tensor has its own generator (its own spawn key), so the bits do not
+    depend on the order or the thread that draws them; numpy's bulk draws and
+    the bf16 rounding release the GIL.
+    """
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=min(8, len(specs))) as ex:
+        futs = {k: ex.submit(normal, *args, **kw) for k, (args, kw) in specs.items()}
+        return {k: f.result() for k, f in futs.items()}
+
+
 def layer_weights(wl: Workload, layer: int = 0) -> dict:
     """One layer's parameters, nn.Linear convention W[out, in].
 
@@ -79,27 +92,27 @@ def layer_weights(wl: Workload, layer: int = 0) -> dict:
     s: LayerShape = wl.shape
     c, dt = wl.cfg_id, s.dtype
     d, dq, dkv, f = s.hidden, s.d_q, s.d_kv, s.ffn
-    return {
-        "attn_norm": normal((d,), WEIGHT_STD, dt, c, layer, T_ATTN_NORM, mean=1.0),
-        "wq": normal((dq, d), WEIGHT_STD, dt, c, layer, T_WQ),
-        "wk": normal((dkv, d), WEIGHT_STD, dt, c, layer, T_WK),
-        "wv": normal((dkv, d), WEIGHT_STD, dt, c, layer, T_WV),
-        "wo": normal((d, dq), WEIGHT_STD, dt, c, layer, T_WO),
-        "ffn_norm": normal((d,), WEIGHT_STD, dt, c, layer, T_FFN_NORM, mean=1.0),
-        "wg": normal((f, d), WEIGHT_STD, dt, c, layer, T_WG),
-        "wu": normal((f, d), WEIGHT_STD, dt, c, layer, T_WU),
-        "wd": normal((d, f), WEIGHT_STD, dt, c, layer, T_WD),
-    }
+    return _draw({
+        "attn_norm": (((d,), WEIGHT_STD, dt, c, layer, T_ATTN_NORM), {"mean": 1.0}),
+        "wq": (((dq, d), WEIGHT_STD, dt, c, layer, T_WQ), {}),
+        "wk": (((dkv, d), WEIGHT_STD, dt, c, layer, T_WK), {}),
+        "wv": (((dkv, d), WEIGHT_STD, dt, c, layer, T_WV), {}),
+        "wo": (((d, dq), WEIGHT_STD, dt, c, layer, T_WO), {}),
+        "ffn_norm": (((d,), WEIGHT_STD, dt, c, layer, T_FFN_NORM), {"mean": 1.0}),
+        "wg": (((f, d), WEIGHT_STD, dt, c, layer, T_WG), {}),
+        "wu": (((f, d), WEIGHT_STD, dt, c, layer, T_WU), {}),
+        "wd": (((d, f), WEIGHT_STD, dt, c, layer, T_WD), {}),
+    })
 
 
 def model_head_weights(wl: Workload) -> dict:
     s = wl.shape
     c, dt = wl.cfg_id, s.dtype
-    return {
-        "embed": normal((wl.vocab, s.hidden), WEIGHT_STD, dt, c, 0, T_EMBED),
-        "final_norm": normal((s.hidden,), WEIGHT_STD, dt, c, 0, T_FINAL_NORM, mean=1.0),
-        "lm_head": normal((wl.vocab, s.hidden), WEIGHT_STD, dt, c, 0, T_LM_HEAD),
-    }
+    return _draw({
+        "embed": (((wl.vocab, s.hidden), WEIGHT_STD, dt, c, 0, T_EMBED), {}),
+        "final_norm": (((s.hidden,), WEIGHT_STD, dt, c, 0, T_FINAL_NORM), {"mean": 1.0}),
+        "lm_head": (((wl.vocab, s.hidden), WEIGHT_STD, dt, c, 0, T_LM_HEAD), {}),
+    })
 
 
 # ---------------------------------------------------------------- activations

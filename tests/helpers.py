@@ -9,12 +9,16 @@ from synth import gen
 
 BF16_TOL_ABS, BF16_TOL_REL = 2e-2, 1e-2      # stage-level bound for bf16 outputs
 F32_TOL_ABS, F32_TOL_REL = 1e-4, 1e-4        # fp32 layer bound
-NORMWISE_TOL = 1e-2                           # end-to-end bf16 layer bound (d <= 4096)
-# d = 8192, F = 28672: an fp32 emulation with bf16 rounding at exactly the
-# device's rounding points (GEMM inputs, q/k/v, P, o, m, layer output) reaches
-# normwise max 1.15e-2 / rms 1.01e-2 against fp64 on the 256-token prompt of
-# the 70B-shaped layer; the end-to-end bound there is 2e-2
-NORMWISE_TOL_70B = 2e-2
+# End-to-end bf16 layer bounds (normwise max|g-r|/max|r| and rms(g-r)/rms(r)).
+# A float32 model with bf16 rounding at exactly the device's rounding points
+# (tests/bf16_emulation.py) sets the floor any such pipeline reaches against
+# the fp64 oracle; a bound is that floor times TOL_MARGIN, which covers the
+# device's different fp32 summation order and the spread of the max-based
+# metric between inputs (tests/test_tolerance.py recomputes the floors).
+TOL_MARGIN = 1.3
+NORMWISE_TOL = 1e-2                           # d = 4096: floor 5.8e-3, so 1e-2 holds with room
+NORMWISE_FLOOR_70B = 1.152e-2                 # d = 8192, F = 28672: the floor on the 256-token prompt
+NORMWISE_TOL_70B = 1.5e-2                     # = 1.3 x 1.152e-2, rounded up
 
 
 def torch_mod():

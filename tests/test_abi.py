@@ -246,3 +246,30 @@ def test_unaligned_device_pointers_are_rejected_before_launch():
     h = c_void_p()
     from ctypes import byref
     assert B.lib.ps_kv_create(byref(cfg), 1, 8, 2, 4, c_void_p(FAKE_POOL + 4), 0, byref(h)) == B.PS_E_INVALID
+
+
+def test_config_match_ignores_struct_padding():
+    """Layer and pool configurations are compared field by field: garbage in
+    the struct's tail padding (a C caller's separately built config) is not a
+    difference, a different field is. No launch happens: the call then stops
+    at the capacity check."""
+    import ctypes
+    sh = CONFIGS["llama8b_decode"].shape
+    clean = B.make_cfg(sh)
+    dirty = B.make_cfg(sh)
+    assert ctypes.sizeof(B.LayerCfg) == 40 and B.LayerCfg.dtype.offset == 32
+    ctypes.memset(ctypes.addressof(dirty) + 36, 0xAB, 4)
+    assert bytes(clean) != bytes(dirty)
+    other = B.make_cfg(sh)
+    other.ffn = sh.ffn * 2
+    kv = B.KV(clean, 1, 64, 4, 16, FAKE_POOL, 0)
+    s = kv.open()
+    kv.alloc(s, 16)
+    fake = 0x100000
+    w = B.LayerW(fake, fake, fake, fake, fake, fake)
+    for cfg, want in ((dirty, B.PS_E_CAPACITY), (other, B.PS_E_INVALID)):
+        layer = B.Layer(cfg)
+        rc = B.lib.ps_prefill(layer.h, ctypes.byref(w), kv.h, 0, 1, B.ints([s]), B.ints([17]), fake, fake, fake,
+                              1 << 30, None)
+        assert rc == want, (rc, B.last_error())
+    assert "differ" in B.last_error()

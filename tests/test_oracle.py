@@ -246,3 +246,91 @@ def test_sequences_are_independent():
 def test_argmax_ties_go_to_lowest_index():
     logits = np.array([[0.0, 3.0, 1.0, 3.0], [5.0, 5.0, 5.0, 5.0]])
     assert list(O.argmax_lowest(logits)) == [1, 0]
+
+
+# ------------------------------------------------------------ model head
+# The model head follows the stack the evaluation serves (§VI: 70B-class
+# Llama-family models): h0 = E[token]; logits = RMSNorm(h_L) * g_final . W_lm^T;
+# next = argmax. Pinned by scalar loops, one-hot / identity-weight closed forms
+# and planted mistakes that the pins must catch.
+def _embed_scalar(table, tokens):
+    rows = table.tolist()
+    return [list(rows[t]) for t in tokens]
+
+
+def _lm_logits_scalar(h, g, w_lm, eps):
+    gl, wl = g.tolist(), w_lm.tolist()
+    out = []
+    for row in h.tolist():
+        ms = 0.0
+        for a in row:
+            ms += a * a
+        inv = 1.0 / math.sqrt(ms / len(row) + eps)
+        hn = [row[i] * inv * gl[i] for i in range(len(row))]
+        logits = []
+        for wr in wl:
+            acc = 0.0
+            for i in range(len(hn)):
+                acc += wr[i] * hn[i]
+            logits.append(acc)
+        out.append(logits)
+    return out
+
+
+def test_embed_is_a_row_gather():
+    r = np.random.default_rng(30)
+    table = r.standard_normal((11, 6))
+    tokens = np.array([3, 0, 10, 3, 7])
+    got = O.embed(table, tokens)
+    np.testing.assert_array_equal(got, np.array(_embed_scalar(table, tokens)))
+    onehot = np.zeros((len(tokens), 11))
+    onehot[np.arange(len(tokens)), tokens] = 1.0
+    np.testing.assert_array_equal(got, onehot @ table)  # E^T e_t, exact with one nonzero term
+    assert got.shape == (5, 6) and np.array_equal(got[0], got[3])
+
+
+def _lm_logits_pins_hold():
+    """True when oracle.lm_logits passes every pin below (used on planted mutants too)."""
+    r = np.random.default_rng(31)
+    d, vocab, eps = 12, 17, 1e-5
+    h = r.standard_normal((3, d)) * 3.0
+    g = 1.0 + 0.3 * r.standard_normal(d)
+    w = r.standard_normal((vocab, d))
+    ok = np.max(np.abs(O.lm_logits(h, g, w, eps) - np.array(_lm_logits_scalar(h, g, w, eps)))) <= 1e-12
+    # identity head, unit gain, eps 0: the logits are the normalised row (RMS exactly 1)
+    z = O.lm_logits(h, np.ones(d), np.eye(d), 0.0)
+    ok = ok and np.allclose(np.sqrt(np.mean(z * z, -1)), 1.0, rtol=1e-13, atol=0)
+    # a final norm makes the head invariant to the scale of h (eps 0)
+    ok = ok and np.allclose(O.lm_logits(7.5 * h, g, w, 0.0), O.lm_logits(h, g, w, 0.0), rtol=1e-12, atol=1e-12)
+    # the gain multiplies before the head: doubling g doubles every logit
+    ok = ok and np.allclose(O.lm_logits(h, 2.0 * g, w, eps), 2.0 * O.lm_logits(h, g, w, eps), rtol=1e-13, atol=0)
+    return bool(ok)
+
+
+def test_lm_logits_pins():
+    assert _lm_logits_pins_hold()
+
+
+@pytest.mark.parametrize("mutant", ["no_final_norm", "no_gain", "eps_outside_sqrt"])
+def test_lm_logits_pins_catch_planted_mistakes(monkeypatch, mutant):
+    """Plant a plausible slip in the oracle's final norm; the pins must fail."""
+    orig = O.rmsnorm
+    if mutant == "no_final_norm":
+        monkeypatch.setattr(O, "rmsnorm", lambda x, g, eps: x * g)
+    elif mutant == "no_gain":
+        monkeypatch.setattr(O, "rmsnorm", lambda x, g, eps: orig(x, np.ones_like(g), eps))
+    else:
+        monkeypatch.setattr(O, "rmsnorm",
+                            lambda x, g, eps: x / (np.sqrt(np.mean(x * x, -1, keepdims=True)) + eps) * g)
+    assert not _lm_logits_pins_hold()
+
+
+@pytest.mark.parametrize("L", [0, 6])
+def test_layer_rows_equals_the_rows_of_layer_sequence(L):
+    shape = LayerShape(32, 4, 2, 8, 48, 1e-5, 10000.0, "f32")
+    w = _weights(shape, 24, 0.1)
+    x = np.random.default_rng(25).standard_normal((9, 32))
+    kh, vh = _hist(shape, L, 26) if L else (None, None)
+    full = O.layer_sequence(w, shape, x, kh, vh)["out"]
+    rows = [8, 0, 4]
+    assert np.max(np.abs(O.layer_rows(w, shape, x, rows, kh, vh) - full[rows])) <= 1e-12
