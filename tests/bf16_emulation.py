@@ -73,9 +73,10 @@ class WidenedWeights:
         return self.bits.keys()
 
 
-def layer(w32: dict, shape, x32: np.ndarray, k_hist=None, v_hist=None) -> np.ndarray:
+def layer(w32: dict, shape, x32: np.ndarray, k_hist=None, v_hist=None, return_kv: bool = False):
     """The layer over the new rows of one sequence (rows at positions L..L+n-1,
-    L = len(k_hist)); history is bf16-valued float32 [L, n_kv, hd]."""
+    L = len(k_hist)); history is bf16-valued float32 [L, n_kv, hd]. With
+    return_kv, also the rounded k and v rows the step appends."""
     n = x32.shape[0]
     nq, nkv, hd = shape.n_q, shape.n_kv, shape.head_dim
     G = nq // nkv
@@ -87,6 +88,7 @@ def layer(w32: dict, shape, x32: np.ndarray, k_hist=None, v_hist=None) -> np.nda
     v = bf(xn @ w32["wv"].T).reshape(n, nkv, hd)
     q = bf(_rope32(q, pos, shape.theta))
     k = bf(_rope32(k, pos, shape.theta))
+    k_new, v_new = k, v
     if L:
         k = np.concatenate([k_hist, k])
         v = np.concatenate([v_hist, v])
@@ -104,4 +106,10 @@ def layer(w32: dict, shape, x32: np.ndarray, k_hist=None, v_hist=None) -> np.nda
     gate = hn @ w32["wg"].T
     up = hn @ w32["wu"].T
     m = bf(gate / (np.float32(1.0) + np.exp(-gate)) * up)
-    return bf(hres + m @ w32["wd"].T)
+    out = bf(hres + m @ w32["wd"].T)
+    return (out, k_new, v_new) if return_kv else out
+
+
+def lm_logits(h32: np.ndarray, g_final32: np.ndarray, w_lm32: np.ndarray, eps: float) -> np.ndarray:
+    """Final RMSNorm rounded to bf16 (the LM head GEMM's input), fp32 logits."""
+    return bf(_rms32(h32, g_final32, eps)) @ w_lm32.T

@@ -13,6 +13,7 @@ import pytest
 from oracle import layer as O
 from synth import gen
 from synth.configs import CONFIGS, LayerShape, Workload
+from tests import bf16_emulation as E
 from tests import helpers as H
 
 pytestmark = pytest.mark.gpu
@@ -213,3 +214,122 @@ def test_model_rejects_shallow_pool():
     with pytest.raises(B.PsError) as e:
         model.prefill(pool.kv, [s], [4], tok, nxt, ws)
     assert e.value.code == B.PS_E_INVALID
+
+
+# ------------------------------------------------------------- 70B width
+def _lm_chunks(h64, g64, lm_bits, eps, dtype, fn, chunk=16384):
+    """Logits over the whole vocabulary, the LM head widened chunk by chunk."""
+    out = []
+    for v0 in range(0, lm_bits.shape[0], chunk):
+        w = gen.bf16_bits_to_f32(lm_bits[v0:v0 + chunk]).astype(dtype)
+        out.append(fn(h64, g64, w, eps))
+    return np.concatenate(out, axis=-1)
+
+
+@pytest.mark.timeout(900)
+def test_70b_width_two_layer_model_full_vocab():
+    """ps_model_prefill and two ps_model_decode_step calls of a 2-layer model
+    at the 70B shape (d 8192, 64 / 8 heads, F 28672) with the full 128256
+    vocabulary, against the fp64 oracle stack (embedding, both layers, final
+    norm, LM head). Weights are drawn on the device by a seeded torch
+    generator and copied to the host as bf16 bits; the oracle widens them.
+
+    Bound: the same stack through the bf16 rounding model on the same inputs
+    gives the error floor of any pipeline with the device's rounding points;
+    the device's logits must be within TOL_MARGIN times that floor (normwise
+    max and rms). Tokens: if every logit is within e of the oracle's, the
+    device's argmax t has oracle logit >= max - 2e, so a token is accepted
+    within 2e with e = the normwise bound times max |logit|."""
+    sh = CONFIGS["llama70b_model"].shape
+    V, L = CONFIGS["llama70b_model"].vocab, 2
+    d, dq, dkv, F = sh.hidden, sh.d_q, sh.d_kv, sh.ffn
+    g = torch.Generator(device="cuda").manual_seed(7070)
+
+    def rn(shape, mean=0.0):
+        t = torch.randn(shape, generator=g, device="cuda") * 0.02
+        return (t + mean).to(torch.bfloat16)
+
+    def host_bits(t):
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    def tiled(w):
+        out = torch.empty(B.tiled_weight_elems(*w.shape), dtype=torch.bfloat16, device="cuda")
+        B.op_tile_weight(B.PS_BF16, w.shape[0], w.shape[1], w, out)
+        return out
+
+    keep, dev_layers, bits = [], [], []
+    for l in range(L):
+        t = {"attn_norm": rn((d,), 1.0), "wq": rn((dq, d)), "wk": rn((dkv, d)), "wv": rn((dkv, d)),
+             "wo": rn((d, dq)), "ffn_norm": rn((d,), 1.0), "wg": rn((F, d)), "wu": rn((F, d)), "wd": rn((d, F))}
+        gu = torch.stack([t["wg"].view(F // 32, 32, d), t["wu"].view(F // 32, 32, d)], 1).reshape(2 * F, d)
+        dev = {"attn_norm": t["attn_norm"], "w_qkv": tiled(torch.cat([t["wq"], t["wk"], t["wv"]])),
+               "w_o": tiled(t["wo"]), "ffn_norm": t["ffn_norm"], "w_gate_up": tiled(gu), "w_down": tiled(t["wd"])}
+        keep.append(dev)
+        dev_layers.append(B.layer_weights(**dev))
+        bits.append({k: host_bits(v) for k, v in t.items()})
+        del t, gu
+    embed, final_norm, lm = rn((V, d)), rn((d,), 1.0), rn((V, d))
+    lm_t = tiled(lm)
+    embed_bits, gfin_bits, lm_bits = host_bits(embed), host_bits(final_norm), host_bits(lm)
+    del lm
+    torch.cuda.synchronize()
+    print("weights on device and host", flush=True)
+
+    lens = [45, 64]
+    pool = H.Pool(sh, 32, 4, 8, n_layers=L, seed=31)
+    model = B.Model(pool.cfg, dev_layers, V, embed, final_norm, lm_t)
+    seqs = [pool.kv.open() for _ in lens]
+    for s, n in zip(seqs, lens):
+        pool.kv.alloc(s, n + 2)
+    ws = H.workspace(B.Model.workspace_bytes(pool.cfg, V, sum(lens), 4, 8))
+    wl = CONFIGS["llama70b_model"]
+    toks = gen.token_ids(wl, sum(lens))
+    nxt = torch.empty(len(seqs), dtype=torch.int32, device="cuda")
+    logits = torch.empty((len(seqs), V), dtype=torch.float32, device="cuda")
+
+    w64 = [E.WidenedWeights(b, np.float64) for b in bits]
+    w32 = [E.WidenedWeights(b, np.float32) for b in bits]
+    g64 = gen.bf16_bits_to_f32(gfin_bits).astype(np.float64)
+    g32 = gen.bf16_bits_to_f32(gfin_bits)
+    hist64 = [[None] * L for _ in lens]   # per sequence, per layer (K, V)
+    hist32 = [[None] * L for _ in lens]
+
+    def run_oracles(i, tokens):
+        h64 = gen.bf16_bits_to_f32(embed_bits[tokens]).astype(np.float64)
+        h32 = gen.bf16_bits_to_f32(embed_bits[tokens])
+        for l in range(L):
+            kh, vh = hist64[i][l] or (None, None)
+            r = O.layer_sequence(w64[l], sh, h64, kh, vh)
+            hist64[i][l] = (r["k"], r["v"]) if kh is None else (np.concatenate([kh, r["k"]]),
+                                                                 np.concatenate([vh, r["v"]]))
+            h64 = r["out"]
+            kh, vh = hist32[i][l] or (None, None)
+            h32, k, v = E.layer(w32[l], sh, h32, kh, vh, return_kv=True)
+            hist32[i][l] = (k, v) if kh is None else (np.concatenate([kh, k]), np.concatenate([vh, v]))
+        ref = _lm_chunks(h64[-1:], g64, lm_bits, sh.eps, np.float64, O.lm_logits)[0]
+        emu = _lm_chunks(h32[-1:], g32, lm_bits, sh.eps, np.float32, E.lm_logits)[0]
+        return ref, emu.astype(np.float64)
+
+    def check(step, tokens_per_seq):
+        torch.cuda.synchronize()
+        got = logits.cpu().numpy().astype(np.float64)
+        refs, emus = zip(*[run_oracles(i, t) for i, t in enumerate(tokens_per_seq)])
+        ref, emu = np.stack(refs), np.stack(emus)
+        floor = max(H.normwise(emu, ref))
+        bound = H.TOL_MARGIN * floor
+        mx, rms = H.normwise(got, ref)
+        print(f"{step}: device normwise max {mx:.3e} rms {rms:.3e}; rounding floor {floor:.3e}", flush=True)
+        assert floor < 5e-2, f"{step}: rounding floor {floor:.3e}"
+        assert mx <= bound and rms <= bound, f"{step}: normwise {mx:.3e} {rms:.3e} > {bound:.3e}"
+        tau = 2 * bound * np.abs(ref).max(axis=1)
+        for i, t in enumerate(nxt.cpu().numpy()):
+            assert ref[i][t] >= ref[i].max() - tau[i], f"{step} row {i}: token {t}"
+
+    model.prefill(pool.kv, seqs, lens, torch.from_numpy(toks).cuda(), nxt, ws, logits)
+    pool.kv.commit(seqs, lens)
+    check("prefill", [toks[:lens[0]], toks[lens[0]:]])
+    for step in range(2):
+        t = gen.token_ids(wl, len(seqs), step=step + 1)
+        model.decode_step(pool.kv, B.PS_PHASE_ANSWER, seqs, torch.from_numpy(t).cuda(), nxt, ws, logits)
+        pool.kv.commit(seqs, [1] * len(seqs))
+        check(f"decode {step}", [t[i:i + 1] for i in range(len(seqs))])

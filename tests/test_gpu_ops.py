@@ -327,8 +327,11 @@ DEC_LENS = [0, 14, 15, 16, 17, 100, 1000, 2500]
 
 
 @pytest.mark.parametrize("shape", [S8, S70], ids=["G4", "G8"])
-@pytest.mark.parametrize("split", [0, 1, 3, 8])
+@pytest.mark.parametrize("split", [0, 1, 3, 8, 20, 33, 64])
 def test_decode_attention(shape, split):
+    """split_pages >= 20 puts more than 16 pages in each wave's range of the
+    longest sequences (157 pages), so the steady-state page ring runs; 0 is
+    the library's choice (at least 8 pages per split)."""
     P = make_pool(shape, 600, 8, 200, seed=77)
     seqs, Ks, Vs = fill_kv(P, DEC_LENS, [1] * len(DEC_LENS), "bf16", 100)
     q = rnd((len(seqs), shape.n_q, shape.head_dim), "bf16", 50)
