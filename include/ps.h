@@ -294,6 +294,25 @@ ps_status ps_op_gemm(int32_t dtype, int32_t r_dtype, int32_t c_dtype, int32_t ep
                      int32_t K, const void* A, const void* W, const void* R, void* C, void* ws, size_t ws_bytes,
                      void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid hipMalloc): ps_op_gemm
+ * without a workspace argument. Decode-sized launches that split K keep
+ * their fp32 partials in a library-owned static device array of
+ * PS_GEMM_STATIC_SCRATCH_BYTES (one copy per GPU, held until the process
+ * ends; its address is looked up once per device on the first call that
+ * needs it). The call allocates nothing. Shapes whose partials would exceed
+ * the array are rejected with PS_E_INVALID before anything is enqueued (the
+ * launch plans write at most 8 MiB of partials, except SwiGLU launches with
+ * N % 128 != 0, which write 4 M N bytes: N up to 65536 fits); a stream of a
+ * device other than the current one is rejected. Every call on
+ * one GPU shares that array: calls that overlap on one GPU (concurrent
+ * streams) race; calls ordered on one stream do not. Each call overwrites
+ * every partial it reads, so nothing carries over between calls. */
+#define PS_GEMM_STATIC_SCRATCH_BYTES (16u << 20)
+ps_status ps_op_gemm_static(int32_t dtype, int32_t r_dtype, int32_t c_dtype, int32_t epilogue, int32_t M,
+                            int32_t N, int32_t K, const void* A, const void* W, const void* R, void* C,
+                            void* stream);
+
 /* RoPE + paged KV write for `layer`: qkv [rows, d_q + 2 d_kv] (cfg.dtype)
  * holds the QKV projection of rows grouped by sequence as in ps_prefill;
  * writes rotated q to q_out [rows, d_q] and rotated k and v into the pages

@@ -93,6 +93,7 @@ _SIGS = {
     "ps_op_gemm_workspace_bytes": (c_size_t, [_I, _I, _I, _I]),
     "ps_op_gemm": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, c_size_t, _P]),
     "ps_op_rope_kvwrite": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
+    "ps_op_gemm_static": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "ps_op_attention": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_op_decode_attention": (_I, [_P, _I, _I, _IP, _P, _P, _I, _P, c_size_t, _P]),
     "ps_op_decode_plan": (_I, [_P, _I, _IP, _I, _P, c_size_t, _P]),
@@ -357,6 +358,12 @@ def op_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, W, R, C, ws=None, stream=None):
     wsb = 0 if ws is None else ws.numel() * ws.element_size()
     check(lib.ps_op_gemm(dtype, r_dt, c_dt, epi, M, N, K, ptr(A), ptr(W), ptr(R), ptr(C), ptr(ws), wsb,
                          stream_handle(stream)))
+
+
+def op_gemm_static(dtype, r_dt, c_dt, epi, M, N, K, A, W, R, C, stream=None):
+    """ps_op_gemm with split-K partials in the library's static device array (no workspace)."""
+    check(lib.ps_op_gemm_static(dtype, r_dt, c_dt, epi, M, N, K, ptr(A), ptr(W), ptr(R), ptr(C),
+                                stream_handle(stream)))
 
 
 def op_rope_kvwrite(kv: KV, layer, seqs, n_tok, qkv, q_out, ws, stream=None):

@@ -1044,6 +1044,42 @@ extern "C" ps_status ps_op_gemm(int32_t dtype, int32_t r_dt, int32_t c_dt, int32
   PS_CATCH
 }
 
+static_assert(kGemmStaticScratchBytes == PS_GEMM_STATIC_SCRATCH_BYTES, "static scratch size");
+
+extern "C" ps_status ps_op_gemm_static(int32_t dtype, int32_t r_dt, int32_t c_dt, int32_t epi, int32_t M, int32_t N,
+                                       int32_t K, const void* A, const void* Wt, const void* R, void* C,
+                                       void* stream) {
+  PS_TRY
+  if (epi < 0 || epi > 2) return fail(PS_E_INVALID, "bad epilogue");
+  if (M > 0 && (!A || !Wt || !C || (epi == 1 && !R))) return fail(PS_E_INVALID, "null pointer");
+  if (ps_status rc = check_aligned({A, Wt, R, C})) return rc;
+  if (gemm_check(dtype, epi, M, N, K)) return fail(PS_E_UNSUPPORTED, "GEMM shape not supported");
+  const size_t need = gemm_partials_bytes(dtype, epi, M, N, K);
+  if (need > PS_GEMM_STATIC_SCRATCH_BYTES)
+    return fail(PS_E_INVALID, "split-K partials need " + std::to_string(need) +
+                                  " bytes, more than the static scratch holds (PS_GEMM_STATIC_SCRATCH_BYTES); "
+                                  "use ps_op_gemm with a workspace");
+  if (M == 0) return PS_OK;
+  hipStream_t st = (hipStream_t)stream;
+  void* scratch = nullptr;
+  if (need) {
+    // the scratch copy is per device: the stream must run on the current one
+    if (st) {
+      int cur = 0, sdev = 0;
+      hipError_t e = hipGetDevice(&cur);
+      if (e == hipSuccess) e = hipStreamGetDevice(st, &sdev);
+      if (e != hipSuccess) return hip_fail(e, "stream device");
+      if (sdev != cur) return fail(PS_E_INVALID, "the stream belongs to another device than the current one");
+    }
+    if (hipError_t e = gemm_static_scratch(&scratch)) return hip_fail(e, "static scratch address");
+  }
+  if (epi != 1) r_dt = 0;
+  int rc = launch_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, Wt, R, C, scratch, need, st);
+  if (rc) return fail(PS_E_UNSUPPORTED, "dtype/epilogue combination not supported");
+  return last_launch_error();
+  PS_CATCH
+}
+
 extern "C" ps_status ps_op_tile_weight(int32_t dtype, int32_t N, int32_t K, const void* w, void* out, void* stream) {
   PS_TRY
   if (!w || !out || N <= 0 || K <= 0 || (dtype != PS_F32 && dtype != PS_BF16))

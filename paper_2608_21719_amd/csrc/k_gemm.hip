@@ -21,6 +21,7 @@
 #include "common.h"
 #include "launch.h"
 
+#include <mutex>
 #include <type_traits>
 
 namespace ps {
@@ -846,6 +847,46 @@ int launch_gemm_split(int dtype, int r_dt, int c_dt, int epi, int M, int N, int 
     }
   }
   return launch_gemm(dtype, r_dt, c_dt, epi, M, N, K, A, W, R, C, ws, ws_bytes, st);
+}
+
+// Bytes of split-K partials a bf16 launch actually writes: 0 for the tile
+// path and for skinny launches that apply their epilogue in the kernel.
+size_t gemm_partials_bytes(int dtype, int epi, int M, int N, int K) {
+  if (dtype != 1 || M <= 0 || M > skinny::MAXM || N % 64 != 0 || K % 64 != 0) return 0;
+  const SkinnyPlan pl = gemm_skinny_plan(M, N, K);
+  if (pl.s == 1 && (epi != 2 || pl.wn == 2)) return 0;
+  return (size_t)pl.s * M * N * sizeof(float);
+}
+
+// ------------------------------------------------------------ static scratch
+// Split-K partials for callers that cannot allocate device memory: a
+// file-scope device array, one copy on every GPU the library runs on, kept
+// until the process ends. In host code `scratch` names a host-side stand-in,
+// not a device address, so host code never passes it to a kernel or a copy:
+// gemm_static_scratch() returns the device address of the current GPU's
+// copy, looked up once per device with hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[kGemmStaticScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+}  // namespace
+
+hipError_t gemm_static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace ps

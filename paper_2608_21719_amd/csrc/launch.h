@@ -49,6 +49,12 @@ struct SkinnyPlan {
 };
 SkinnyPlan gemm_skinny_plan(int M, int N, int K);
 int gemm_check(int dtype, int epi, int M, int N, int K);
+// Split-K partial bytes a launch really uses (0 when nothing is split).
+size_t gemm_partials_bytes(int dtype, int epi, int M, int N, int K);
+// Size of the static split-K scratch array (PS_GEMM_STATIC_SCRATCH_BYTES).
+constexpr size_t kGemmStaticScratchBytes = size_t(16) << 20;
+// Device address of the current GPU's copy of that array.
+hipError_t gemm_static_scratch(void** out);
 
 // model-level kernels (bf16 rows)
 // One metadata upload: n16 16-byte units from mapped host memory (src) to

@@ -273,3 +273,17 @@ def test_config_match_ignores_struct_padding():
                               1 << 30, None)
         assert rc == want, (rc, B.last_error())
     assert "differ" in B.last_error()
+
+
+def test_static_gemm_rejects_partials_beyond_its_scratch_on_the_host():
+    """ps_op_gemm_static checks the split-K partials against its static array
+    before touching the device (no GPU here): a SwiGLU launch on one 64-row
+    block per workgroup without a K split writes 4 M N bytes of partials."""
+    from ctypes import c_void_p
+    p = c_void_p(0x100000)
+    M, N, K = 64, 64 * 1025, 64
+    assert 4 * M * N > 16 << 20
+    rc = B.lib.ps_op_gemm_static(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_SWIGLU, M, N, K, p, p, None, p, None)
+    assert rc == B.PS_E_INVALID and "static scratch" in B.last_error()
+    rc = B.lib.ps_op_gemm_static(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_STORE, 256, 100, 64, p, p, None, p, None)
+    assert rc == B.PS_E_UNSUPPORTED
