@@ -193,6 +193,22 @@ ps_status ps_kv_append(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* 
 ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k_out, void* v_out, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* Think -> answer handoff between two pools (§IV-A: a reasoning request's
+ * think and answer stages run on their own pools; §V "What does KV transfer
+ * cost": each such request moves its KV state once, think to answer). Copies
+ * positions [0, len) of src_seq, every layer, from pool `src` into dst_seq of
+ * pool `dst` and makes len the destination's committed length. Both pools
+ * live on the current GPU and have the same configuration and layer count;
+ * dst_seq must be open, empty and have capacity >= len reserved (ps_kv_alloc:
+ * the answer stage's reservation), else PS_E_INVALID / PS_E_CAPACITY with
+ * nothing changed. Pages are copied whole through both block tables, so the
+ * copy is bit-exact whatever either pool's page placement; `ws` holds the two
+ * page lists (8 bytes per page). The source keeps its pages: free them once
+ * any later writer of those pages is ordered after the copy. src may equal
+ * dst (a copy into another sequence of the same pool). */
+ps_status ps_kv_transfer(ps_kv* src, int32_t src_seq, ps_kv* dst, int32_t dst_seq, void* ws, size_t ws_bytes,
+                         void* stream);
+
 /* ------------------------------------------------------------------ layer */
 ps_status ps_layer_create(const ps_layer_cfg* cfg, ps_layer** out);
 ps_status ps_layer_destroy(ps_layer* layer);

@@ -83,6 +83,7 @@ _SIGS = {
     "ps_kv_block_table": (_I, [_P, _I, _IP, _I, _IP]),
     "ps_kv_append": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_kv_gather": (_I, [_P, _I, _I, _P, _P, _P, c_size_t, _P]),
+    "ps_kv_transfer": (_I, [_P, _I, _P, _I, _P, c_size_t, _P]),
     "ps_layer_create": (_I, [POINTER(LayerCfg), POINTER(c_void_p)]),
     "ps_layer_destroy": (_I, [_P]),
     "ps_workspace_bytes": (c_size_t, [POINTER(LayerCfg), _I, _I, _I]),
@@ -92,6 +93,7 @@ _SIGS = {
     "ps_op_rmsnorm": (_I, [_I, _I, _I, _I, _I, _P, _P, c_float, _P, _P]),
     "ps_op_gemm_workspace_bytes": (c_size_t, [_I, _I, _I, _I]),
     "ps_op_gemm": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, c_size_t, _P]),
+    "ps_op_gemm_static": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "ps_op_rope_kvwrite": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_op_gemm_static": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "ps_op_attention": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
@@ -260,6 +262,12 @@ class KV:
     def gather(self, layer, seq, k_out, v_out, ws, stream=None):
         check(lib.ps_kv_gather(self.h, layer, seq, ptr(k_out), ptr(v_out), ptr(ws),
                                ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def kv_transfer(src: KV, src_seq: int, dst: KV, dst_seq: int, ws, stream=None):
+    """Copy a sequence's KV state (every layer) from pool src to pool dst (think -> answer handoff)."""
+    check(lib.ps_kv_transfer(src.h, src_seq, dst.h, dst_seq, ptr(ws), ws.numel() * ws.element_size(),
+                             stream_handle(stream)))
 
 
 class Layer:

@@ -620,6 +620,46 @@ extern "C" ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k
   PS_CATCH
 }
 
+namespace {
+ps_status upload_meta(ps_kv* kv, const Meta& mt, void* ws, hipStream_t st);
+}  // namespace
+
+extern "C" ps_status ps_kv_transfer(ps_kv* src, int32_t src_seq, ps_kv* dst, int32_t dst_seq, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  PS_TRY
+  if (!src || !dst) return fail(PS_E_INVALID, "null kv handle");
+  if (!same_cfg(src->cfg, dst->cfg)) return fail(PS_E_INVALID, "source and destination pool configurations differ");
+  if (src->n_layers != dst->n_layers) return fail(PS_E_INVALID, "source and destination pools differ in layer count");
+  std::string e;
+  if (int rc = src->meta.check_open(src_seq, e)) return fail(rc, "source: " + e);
+  if (int rc = dst->meta.check_open(dst_seq, e)) return fail(rc, "destination: " + e);
+  if (src == dst && src_seq == dst_seq) return fail(PS_E_INVALID, "source and destination are the same sequence");
+  const int32_t len = src->meta.seq(src_seq).len;
+  if (dst->meta.seq(dst_seq).len != 0) return fail(PS_E_INVALID, "destination sequence is not empty");
+  if (int rc = dst->meta.check_writable(dst_seq, len, e)) return fail(rc, "destination: " + e);
+  const int32_t pages = (len + PS_PAGE_TOKENS - 1) / PS_PAGE_TOKENS;
+  Meta mt;
+  const size_t o_sb = mt.add(src->meta.seq(src_seq).pages.data(), (size_t)pages * 4);
+  const size_t o_db = mt.add(dst->meta.seq(dst_seq).pages.data(), (size_t)pages * 4);
+  if (ps_status rc = check_ws(ws, ws_bytes, mt.size())) return rc;
+  if (len > 0) {
+    hipStream_t st = (hipStream_t)stream;
+    if (ps_status rc = upload_meta(dst, mt, ws, st)) return rc;
+    const ps_layer_cfg& c = src->cfg;
+    const size_t eb = elt_bytes(c.dtype);
+    const size_t page_bytes = (size_t)c.n_kv_heads * 2 * PS_PAGE_TOKENS * c.head_dim * eb;
+    if (launch_kv_copy_pages(page_bytes, pages, src->n_layers, src->pool, src->layer_elts * eb,
+                             (const int32_t*)((char*)ws + o_sb), dst->pool, dst->layer_elts * eb,
+                             (const int32_t*)((char*)ws + o_db), st))
+      return fail(PS_E_UNSUPPORTED, "page copy configuration not supported");
+    if (ps_status rc = last_launch_error()) return rc;
+  }
+  // the copied positions become the destination's committed length
+  if (int rc = dst->meta.commit(1, &dst_seq, &len, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+
 // ------------------------------------------------------------------ layer
 extern "C" ps_status ps_layer_create(const ps_layer_cfg* c, ps_layer** out) {
   PS_TRY

@@ -579,4 +579,30 @@ int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt,
   return 0;
 }
 
+// ---------------------------------------------------------------- transfer
+// Whole pages of one sequence, every layer, from one pool to another: block
+// (p, l) copies logical page p of layer l (all KV heads, K and V^T) from the
+// source's physical page src_bt[p] to the destination's dst_bt[p]. Pools may
+// have different page counts, hence their own layer strides. 16-byte copies.
+__global__ __launch_bounds__(256) void kv_copy_pages_kernel(const uint4* __restrict__ src, long src_layer16,
+                                                            const int32_t* __restrict__ src_bt,
+                                                            uint4* __restrict__ dst, long dst_layer16,
+                                                            const int32_t* __restrict__ dst_bt, int page16) {
+  const int p = blockIdx.x, l = blockIdx.y;
+  const uint4* s = src + l * src_layer16 + (long)src_bt[p] * page16;
+  uint4* d = dst + l * dst_layer16 + (long)dst_bt[p] * page16;
+  for (int i = threadIdx.x; i < page16; i += 256) d[i] = s[i];
+}
+
+int launch_kv_copy_pages(size_t page_bytes, int n_pages, int n_layers, const void* src_pool, size_t src_layer_bytes,
+                         const int32_t* src_bt, void* dst_pool, size_t dst_layer_bytes, const int32_t* dst_bt,
+                         hipStream_t st) {
+  if (n_pages == 0 || n_layers == 0) return 0;
+  if (page_bytes % 16 || src_layer_bytes % 16 || dst_layer_bytes % 16 || n_layers > 65535) return -1;
+  hipLaunchKernelGGL(kv_copy_pages_kernel, dim3(n_pages, n_layers), dim3(256), 0, st, (const uint4*)src_pool,
+                     (long)(src_layer_bytes / 16), src_bt, (uint4*)dst_pool, (long)(dst_layer_bytes / 16), dst_bt,
+                     (int)(page_bytes / 16));
+  return 0;
+}
+
 }  // namespace ps

@@ -23,6 +23,12 @@ int launch_split_residual_rmsnorm(int rows, int d, int S, const float* part, con
                                   const void* g, float eps, void* y, hipStream_t st);
 int launch_kv_append(int dt, int rows, const void* k, const void* v, void* pool_layer, const SeqInfo* si,
                      const int32_t* bt, int n_seqs, int n_kv, int hd, hipStream_t st);
+// Pages [0, n_pages) of one sequence, all n_layers layers, copied whole from
+// src_pool (its page ids src_bt) to dst_pool (dst_bt); page_bytes per page
+// and layer, each pool's layer stride in bytes.
+int launch_kv_copy_pages(size_t page_bytes, int n_pages, int n_layers, const void* src_pool, size_t src_layer_bytes,
+                         const int32_t* src_bt, void* dst_pool, size_t dst_layer_bytes, const int32_t* dst_bt,
+                         hipStream_t st);
 int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt, void* k_out, void* v_out,
                      int n_kv, int hd, hipStream_t st);
 

@@ -287,3 +287,39 @@ def test_static_gemm_rejects_partials_beyond_its_scratch_on_the_host():
     assert rc == B.PS_E_INVALID and "static scratch" in B.last_error()
     rc = B.lib.ps_op_gemm_static(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_STORE, 256, 100, 64, p, p, None, p, None)
     assert rc == B.PS_E_UNSUPPORTED
+
+
+def test_kv_transfer_validates_on_the_host():
+    """Every refusal happens before any device work (no GPU here) and leaves
+    both pools unchanged."""
+    sh = CONFIGS["llama8b_decode"].shape
+    src = B.KV(B.make_cfg(sh), 2, 64, 4, 16, FAKE_POOL, 3)
+    dst = B.KV(B.make_cfg(sh), 2, 40, 4, 16, FAKE_POOL, 9)
+    s = src.open()
+    src.alloc(s, 40)
+    src.commit([s], [37])
+    ws = np.zeros(1 << 12, np.uint8)
+
+    def xfer(a, sa, b, sb):
+        return B.lib.ps_kv_transfer(a.h, sa, b.h, sb, ws.ctypes.data, ws.nbytes, None)
+
+    d = dst.open()
+    dst.alloc(d, 32)  # 2 pages: too few for 37 tokens
+    assert xfer(src, s, dst, d) == B.PS_E_CAPACITY and "destination" in B.last_error()
+    assert xfer(src, s, dst, 3) == B.PS_E_INVALID          # destination not open
+    assert xfer(src, 2, dst, d) == B.PS_E_INVALID          # source not open
+    assert xfer(src, s, src, s) == B.PS_E_INVALID          # same sequence
+    other = B.make_cfg(sh)
+    other.n_kv_heads = 4
+    odd = B.KV(other, 2, 40, 4, 16, FAKE_POOL, 0)
+    o = odd.open()
+    odd.alloc(o, 64)
+    assert xfer(src, s, odd, o) == B.PS_E_INVALID and "configurations differ" in B.last_error()
+    shallow = B.KV(B.make_cfg(sh), 1, 40, 4, 16, FAKE_POOL, 0)
+    t = shallow.open()
+    shallow.alloc(t, 64)
+    assert xfer(src, s, shallow, t) == B.PS_E_INVALID and "layer count" in B.last_error()
+    dst.alloc(d, 48)
+    dst.commit([d], [1])
+    assert xfer(src, s, dst, d) == B.PS_E_INVALID and "not empty" in B.last_error()
+    assert src.seq_len(s) == 37 and dst.seq_len(d) == 1 and dst.capacity(d) == 48
