@@ -116,6 +116,22 @@ typedef struct ps_layer ps_layer;
 const char* ps_last_error(void);
 const char* ps_version(void);
 
+/* What the HIP runtime reports for one device (hipGetDeviceProperties), for
+ * deriving roofline peaks on the machine at hand: the paper's roofline
+ * argument (§III-B) prices work against the device's own compute and memory
+ * peaks. Host-only; PS_E_HIP when the runtime has no such device. */
+typedef struct {
+  int32_t compute_units;      /* multiProcessorCount                        */
+  int32_t clock_khz;          /* peak engine clock                          */
+  int32_t memory_clock_khz;   /* peak memory clock                          */
+  int32_t memory_bus_bits;    /* memory bus width                           */
+  int64_t total_memory;       /* bytes                                      */
+  int32_t l2_bytes;
+  int32_t lds_bytes_per_block;
+  char arch[64];              /* gcnArchName, NUL-terminated                */
+} ps_device_info;
+ps_status ps_get_device_info(int32_t device, ps_device_info* out);
+
 /* Host helper: interleave Wg [F, d] and Wu [F, d] (host memory, elt_bytes
  * per element) into the w_gate_up row order above; out has 2F*d elements.
  * Pure layout, no arithmetic. F must be a multiple of PS_GATE_UP_BLOCK. */
@@ -208,6 +224,52 @@ ps_status ps_kv_gather(ps_kv* kv, int32_t layer, int32_t seq, void* k_out, void*
  * dst (a copy into another sequence of the same pool). */
 ps_status ps_kv_transfer(ps_kv* src, int32_t src_seq, ps_kv* dst, int32_t dst_seq, void* ws, size_t ws_bytes,
                          void* stream);
+
+/* ------------------------------------------------------------- admission
+ * Per-stage KV reservation and admission for one stage pool (a ps_kv). Each
+ * stage reserves its own KV "chunk size" per request in tokens (§IV-A: CS_T
+ * for think, CS_A for answer; §III-B's design-space table: 512 / 1024 /
+ * 2048), and PSRoute sets it from the lengths the stage actually produced,
+ * admitting by observation instead of predicting lengths (§IV-D "PSRoute:
+ * adaptive admission instead of prediction"):
+ *   CS_i = mean of the last `window` completed requests' stage lengths,
+ *          rounded up to a page and clamped to [cs_min, cs_max]
+ *          (cs_initial before the first completion);
+ *   admit: a request with ctx tokens of context is admitted iff a sequence
+ *          slot is free and the free pages cover ctx + CS_i tokens, which
+ *          are reserved (ps_kv_alloc) for a new sequence;
+ *   grow:  a running sequence that outgrows its reservation takes further
+ *          whole chunks of the current CS_i; when the pool cannot cover them
+ *          the most recently admitted sequence is preempted (pages freed,
+ *          its request goes back to the caller's queue) -- the KV thrashing
+ *          the adaptive chunk size keeps rare;
+ *   finish: the request's stage length joins the window; its pages are freed.
+ * The scheduler decides and reserves (host only); the caller runs the steps
+ * and commits lengths with ps_kv_commit. It manages only the sequences it
+ * admitted. cs_initial, cs_min and cs_max are positive multiples of 16,
+ * cs_min <= cs_max, window >= 1. Not thread-safe. */
+typedef struct ps_sched ps_sched;
+typedef struct {
+  int32_t window;
+  int32_t cs_initial;
+  int32_t cs_min;
+  int32_t cs_max;
+} ps_sched_cfg;
+ps_status ps_sched_create(ps_kv* kv, const ps_sched_cfg* cfg, ps_sched** out);
+ps_status ps_sched_destroy(ps_sched* s);
+ps_status ps_sched_chunk_size(const ps_sched* s, int32_t* cs);
+ps_status ps_sched_running(const ps_sched* s, int32_t* n);
+/* *seq = the admitted sequence, or -1 (not admitted, nothing changed);
+ * PS_E_CAPACITY when ctx + CS_i exceeds max_pages_per_seq pages. */
+ps_status ps_sched_admit(ps_sched* s, int32_t ctx_tokens, int32_t* seq);
+/* Before a step adding n_tok[i] tokens to seqs[i]: extends reservations,
+ * preempting as needed; writes the preempted (freed) sequence ids, in
+ * preemption order, to `preempted` (room for cap >= the pool's max_seqs ids)
+ * and their number to *n_preempted. Never fails for lack of pages; validates
+ * every argument before changing anything. */
+ps_status ps_sched_reserve_step(ps_sched* s, int32_t n, const int32_t* seqs, const int32_t* n_tok,
+                                int32_t* preempted, int32_t cap, int32_t* n_preempted);
+ps_status ps_sched_finish(ps_sched* s, int32_t seq, int32_t stage_tokens);
 
 /* ------------------------------------------------------------------ layer */
 ps_status ps_layer_create(const ps_layer_cfg* cfg, ps_layer** out);

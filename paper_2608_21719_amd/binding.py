@@ -38,6 +38,16 @@ class LayerCfg(ctypes.Structure):
                 ("ffn", c_int32), ("rms_eps", c_float), ("rope_theta", c_double), ("dtype", c_int32)]
 
 
+class DeviceInfo(ctypes.Structure):
+    _fields_ = [("compute_units", c_int32), ("clock_khz", c_int32), ("memory_clock_khz", c_int32),
+                ("memory_bus_bits", c_int32), ("total_memory", ctypes.c_int64), ("l2_bytes", c_int32),
+                ("lds_bytes_per_block", c_int32), ("arch", ctypes.c_char * 64)]
+
+
+class SchedCfg(ctypes.Structure):
+    _fields_ = [("window", c_int32), ("cs_initial", c_int32), ("cs_min", c_int32), ("cs_max", c_int32)]
+
+
 class LayerW(ctypes.Structure):
     _fields_ = [("attn_norm", c_void_p), ("w_qkv", c_void_p), ("w_o", c_void_p), ("ffn_norm", c_void_p),
                 ("w_gate_up", c_void_p), ("w_down", c_void_p)]
@@ -65,6 +75,7 @@ _IP = POINTER(c_int32)
 _SIGS = {
     "ps_last_error": (c_char_p, []),
     "ps_version": (c_char_p, []),
+    "ps_get_device_info": (_I, [_I, POINTER(DeviceInfo)]),
     "ps_pack_gate_up": (_I, [_P, _P, _I, _I, _I, _P]),
     "ps_tiled_weight_elems": (c_size_t, [_I, _I]),
     "ps_tile_weight": (_I, [_P, _I, _I, _I, _P]),
@@ -84,6 +95,13 @@ _SIGS = {
     "ps_kv_append": (_I, [_P, _I, _I, _IP, _IP, _P, _P, _P, c_size_t, _P]),
     "ps_kv_gather": (_I, [_P, _I, _I, _P, _P, _P, c_size_t, _P]),
     "ps_kv_transfer": (_I, [_P, _I, _P, _I, _P, c_size_t, _P]),
+    "ps_sched_create": (_I, [_P, POINTER(SchedCfg), POINTER(c_void_p)]),
+    "ps_sched_destroy": (_I, [_P]),
+    "ps_sched_chunk_size": (_I, [_P, _IP]),
+    "ps_sched_running": (_I, [_P, _IP]),
+    "ps_sched_admit": (_I, [_P, _I, _IP]),
+    "ps_sched_reserve_step": (_I, [_P, _I, _IP, _IP, _IP, _I, _IP]),
+    "ps_sched_finish": (_I, [_P, _I, _I]),
     "ps_layer_create": (_I, [POINTER(LayerCfg), POINTER(c_void_p)]),
     "ps_layer_destroy": (_I, [_P]),
     "ps_workspace_bytes": (c_size_t, [POINTER(LayerCfg), _I, _I, _I]),
@@ -120,6 +138,12 @@ def last_error() -> str:
 def check(rc: int):
     if rc != PS_OK:
         raise PsError(rc, last_error())
+
+
+def device_info(device: int = 0) -> dict:
+    info = DeviceInfo()
+    check(lib.ps_get_device_info(device, ctypes.byref(info)))
+    return {f: (getattr(info, f).decode() if f == "arch" else getattr(info, f)) for f, _ in DeviceInfo._fields_}
 
 
 def ints(seq):
@@ -268,6 +292,54 @@ def kv_transfer(src: KV, src_seq: int, dst: KV, dst_seq: int, ws, stream=None):
     """Copy a sequence's KV state (every layer) from pool src to pool dst (think -> answer handoff)."""
     check(lib.ps_kv_transfer(src.h, src_seq, dst.h, dst_seq, ptr(ws), ws.numel() * ws.element_size(),
                              stream_handle(stream)))
+
+
+class Sched:
+    """Per-stage KV reservation and admission by observed lengths over one pool."""
+
+    def __init__(self, kv: KV, window: int, cs_initial: int, cs_min: int, cs_max: int):
+        self.kv = kv
+        self.cfg = SchedCfg(window, cs_initial, cs_min, cs_max)
+        h = c_void_p()
+        check(lib.ps_sched_create(kv.h, ctypes.byref(self.cfg), ctypes.byref(h)))
+        self.h = h
+        self._cap = 0
+
+    def close(self):
+        if self.h:
+            check(lib.ps_sched_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def chunk_size(self) -> int:
+        v = c_int32()
+        check(lib.ps_sched_chunk_size(self.h, ctypes.byref(v)))
+        return v.value
+
+    def running(self) -> int:
+        v = c_int32()
+        check(lib.ps_sched_running(self.h, ctypes.byref(v)))
+        return v.value
+
+    def admit(self, ctx_tokens: int):
+        """Sequence id, or None when the request does not fit now."""
+        v = c_int32()
+        check(lib.ps_sched_admit(self.h, ctx_tokens, ctypes.byref(v)))
+        return None if v.value < 0 else v.value
+
+    def reserve_step(self, seqs, n_tok, max_seqs: int):
+        buf = (c_int32 * max(1, max_seqs))()
+        n = c_int32()
+        check(lib.ps_sched_reserve_step(self.h, len(seqs), ints(seqs), ints(n_tok), buf, max_seqs, ctypes.byref(n)))
+        return list(buf[:n.value])
+
+    def finish(self, seq: int, stage_tokens: int):
+        check(lib.ps_sched_finish(self.h, seq, stage_tokens))
 
 
 class Layer:

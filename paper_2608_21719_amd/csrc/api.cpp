@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "../../include/ps.h"
+#include "admission.h"
 #include "common.h"
 #include "kv_pool.h"
 #include "launch.h"
@@ -236,7 +237,25 @@ struct ps_model {
 
 // ------------------------------------------------------------------ misc
 extern "C" const char* ps_last_error(void) { return g_err.c_str(); }
-extern "C" const char* ps_version(void) { return "libps 0.1.0 gfx950"; }
+extern "C" const char* ps_version(void) { return "libps 0.2.0 gfx950"; }
+
+extern "C" ps_status ps_get_device_info(int32_t device, ps_device_info* out) {
+  PS_TRY
+  if (!out) return fail(PS_E_INVALID, "null out");
+  hipDeviceProp_t p;
+  if (hipError_t e = hipGetDeviceProperties(&p, device)) return hip_fail(e, "hipGetDeviceProperties");
+  std::memset(out, 0, sizeof(*out));
+  out->compute_units = p.multiProcessorCount;
+  out->clock_khz = p.clockRate;
+  out->memory_clock_khz = p.memoryClockRate;
+  out->memory_bus_bits = p.memoryBusWidth;
+  out->total_memory = (int64_t)p.totalGlobalMem;
+  out->l2_bytes = p.l2CacheSize;
+  out->lds_bytes_per_block = (int32_t)p.sharedMemPerBlock;
+  std::strncpy(out->arch, p.gcnArchName, sizeof(out->arch) - 1);
+  return PS_OK;
+  PS_CATCH
+}
 
 extern "C" ps_status ps_pack_gate_up(const void* wg, const void* wu, int32_t F, int32_t d, int32_t eb, void* out) {
   PS_TRY
@@ -656,6 +675,70 @@ extern "C" ps_status ps_kv_transfer(ps_kv* src, int32_t src_seq, ps_kv* dst, int
   }
   // the copied positions become the destination's committed length
   if (int rc = dst->meta.commit(1, &dst_seq, &len, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+
+// ------------------------------------------------------------ admission
+struct ps_sched {
+  ps_kv* kv;
+  Admission adm;
+  ps_sched(ps_kv* k, const ps_sched_cfg& c) : kv(k), adm(k->meta, c.window, c.cs_initial, c.cs_min, c.cs_max) {}
+};
+
+extern "C" ps_status ps_sched_create(ps_kv* kv, const ps_sched_cfg* c, ps_sched** out) {
+  PS_TRY CHECK_KV(kv);
+  if (!c || !out) return fail(PS_E_INVALID, "null argument");
+  auto page_multiple = [](int32_t v) { return v > 0 && v % PS_PAGE_TOKENS == 0; };
+  if (c->window < 1 || !page_multiple(c->cs_initial) || !page_multiple(c->cs_min) || !page_multiple(c->cs_max) ||
+      c->cs_min > c->cs_max)
+    return fail(PS_E_INVALID, "window >= 1 and positive chunk sizes in multiples of 16 with cs_min <= cs_max");
+  *out = new ps_sched(kv, *c);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_sched_destroy(ps_sched* s) {
+  PS_TRY
+  delete s;
+  return PS_OK;
+  PS_CATCH
+}
+#define CHECK_SCHED(s) \
+  if (!(s)) return fail(PS_E_INVALID, "null scheduler handle");
+extern "C" ps_status ps_sched_chunk_size(const ps_sched* s, int32_t* cs) {
+  PS_TRY CHECK_SCHED(s);
+  if (!cs) return fail(PS_E_INVALID, "null cs");
+  *cs = s->adm.chunk_size();
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_sched_running(const ps_sched* s, int32_t* n) {
+  PS_TRY CHECK_SCHED(s);
+  if (!n) return fail(PS_E_INVALID, "null n");
+  *n = s->adm.running();
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_sched_admit(ps_sched* s, int32_t ctx, int32_t* seq) {
+  PS_TRY CHECK_SCHED(s);
+  if (!seq) return fail(PS_E_INVALID, "null seq");
+  std::string e;
+  if (int rc = s->adm.admit(ctx, seq, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_sched_reserve_step(ps_sched* s, int32_t n, const int32_t* seqs, const int32_t* n_tok,
+                                           int32_t* preempted, int32_t cap, int32_t* n_preempted) {
+  PS_TRY CHECK_SCHED(s);
+  std::string e;
+  if (int rc = s->adm.reserve_step(n, seqs, n_tok, cap, preempted, n_preempted, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_sched_finish(ps_sched* s, int32_t seq, int32_t stage_tokens) {
+  PS_TRY CHECK_SCHED(s);
+  std::string e;
+  if (int rc = s->adm.finish(seq, stage_tokens, e)) return fail(rc, e);
   return PS_OK;
   PS_CATCH
 }

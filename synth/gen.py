@@ -176,3 +176,20 @@ def page_order_seed(wl: Workload) -> int:
     if not wl.shuffled_pages:
         return 0
     return int(rng(wl.cfg_id, 0, T_PAGE_SEED).integers(1, 2**63 - 1))
+
+
+# ---------------------------------------------------------------- request traces
+def request_trace(seed: int, n: int, rate: float, ctx_range=(32, 512), median: float = 300.0,
+                  sigma: float = 1.0, len_range=(16, 4000)):
+    """Synthetic arrivals for one stage pool: arrival step (Poisson, `rate`
+    per step), context tokens already held (uniform integers in ctx_range)
+    and the tokens the stage will produce (log-normal, heavy-tailed like the
+    reasoning lengths the paper describes, rounded and clipped to len_range).
+    Random draws only."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(BASE_SEED, spawn_key=(99, seed))))
+    gaps = g.exponential(1.0 / rate, size=n)
+    arrival = np.floor(np.cumsum(gaps)).astype(np.int64)
+    ctx = g.integers(ctx_range[0], ctx_range[1] + 1, size=n).astype(np.int64)
+    raw = np.exp(np.log(median) + sigma * g.standard_normal(n))
+    length = np.clip(np.rint(raw), len_range[0], len_range[1]).astype(np.int64)
+    return arrival, ctx, length

@@ -252,3 +252,48 @@ def test_8b_decode_step_equals_composed_stage_ops_bit_for_bit(h8, batch):
         sync()
         np.testing.assert_array_equal(H.bits(got[0][0]), H.bits(got[1][0]))
         np.testing.assert_array_equal(H.bits(got[0][1]), H.bits(got[1][1]))
+
+
+def test_admitted_mixed_batch_matches_oracle():
+    """A batch formed by the admission scheduler (per-stage chunk reservation
+    by observed lengths): two requests admitted and prefilled earlier decode
+    while two newly admitted prompts run as chunk rows of one mixed step,
+    after the scheduler reserved the step's growth. The scheduler decides and
+    reserves on the host; the layer runs on the GPU against the oracle."""
+    wl = CONFIGS["llama8b_think"]
+    h = Harness(wl, n_pages=200, max_seqs=8, max_pages=64, seed=4242)
+    sched = B.Sched(h.kv, 4, 256, 64, 1024)
+    sh = h.shape
+    first = [sched.admit(L) for L in (100, 37)]
+    assert None not in first and sched.chunk_size() == 256
+    for s, L in zip(first, (100, 37)):
+        assert h.kv.capacity(s) >= L + 256
+        h.hist[s] = (np.zeros((0, sh.n_kv, sh.head_dim)), np.zeros((0, sh.n_kv, sh.head_dim)))
+    xp = gen.prefill_input(wl, 137, step=5)
+    h.prefill(first, [100, 37], xp)
+    xpf = gen.widen(xp, "bf16")
+    h.oracle(first[0], xpf[:100])
+    h.oracle(first[1], xpf[100:137])
+    # a completion elsewhere in the stage moves CS_i before the next admissions
+    done = sched.admit(0)
+    sched.finish(done, 90)
+    assert sched.chunk_size() == 96
+    new = [sched.admit(L) for L in (64, 48)]
+    assert None not in new
+    for s in new:
+        h.hist[s] = (np.zeros((0, sh.n_kv, sh.head_dim)), np.zeros((0, sh.n_kv, sh.head_dim)))
+    assert sched.reserve_step(first, [1, 1], 8) == []
+    xm = gen.mixed_input(wl, 64 + 48 + 2)
+    xmf = gen.widen(xm, "bf16")
+    out = H.empty((114, sh.hidden), "bf16")
+    h.layer.mixed_step(h.dev.w, h.kv, 0, new, [64, 48], first, H.to_dev(xm, "bf16"), out, h.ws)
+    h.kv.commit(new + first, [64, 48, 1, 1])
+    sync()
+    got = H.to_f64(out)
+    check(got[:64], h.oracle(new[0], xmf[:64]), "bf16", "admitted chunk 0")
+    check(got[64:112], h.oracle(new[1], xmf[64:112]), "bf16", "admitted chunk 1")
+    check(got[112:113], h.oracle(first[0], xmf[112:113]), "bf16", "running decode 0")
+    check(got[113:114], h.oracle(first[1], xmf[113:114]), "bf16", "running decode 1")
+    for s, n in zip(first + new, (1, 1, 64, 48)):
+        sched.finish(s, n)
+    assert sched.running() == 0 and h.kv.free_pages() == 200
