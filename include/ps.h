@@ -271,6 +271,68 @@ ps_status ps_sched_reserve_step(ps_sched* s, int32_t n, const int32_t* seqs, con
                                 int32_t* preempted, int32_t cap, int32_t* n_preempted);
 ps_status ps_sched_finish(ps_sched* s, int32_t seq, int32_t stage_tokens);
 
+/* ------------------------------------------------------ frequency control
+ * Vote-commit DVFS daemon, one per GPU (§V "How is GPU frequency actually
+ * set", Alg. 1): a request entering a stage votes (target frequency f*,
+ * SLO-class weight w); leaving retracts the vote. Each tick picks, over the
+ * DVFS ladder, the frequency maximising sum_votes w * b(f; f*) with
+ *   b(f; f*) = -(under_weight * max(0, f* - f) + over_weight * max(0, f - f*))
+ * (running below a target risks the SLO, above it wastes power; ties take the
+ * lower frequency; no votes give the lowest), calls `lock` only when the
+ * choice changed, and calls `limit` with the power cap every tick (the
+ * hardware backstop). The actuators are caller callbacks (a clock lock and a
+ * power limit through the platform's management library, or test fakes);
+ * they must not call back into the daemon, and return 0 on success.
+ * ps_dvfs_start runs ticks on a background thread every period_ms (the
+ * paper's 50-100 ms); ps_dvfs_stop joins it. Votes may come from any thread.
+ * ladder_mhz is strictly increasing. Returns PS_E_HIP if an actuator failed. */
+typedef int32_t (*ps_dvfs_lock_fn)(void* ctx, int32_t mhz);
+typedef int32_t (*ps_dvfs_limit_fn)(void* ctx, int32_t watts);
+typedef struct ps_dvfs ps_dvfs;
+ps_status ps_dvfs_create(const int32_t* ladder_mhz, int32_t n, double under_weight, double over_weight,
+                         int32_t power_limit_w, int32_t initial_mhz, ps_dvfs_lock_fn lock, ps_dvfs_limit_fn limit,
+                         void* ctx, ps_dvfs** out);
+ps_status ps_dvfs_destroy(ps_dvfs* d);
+ps_status ps_dvfs_vote(ps_dvfs* d, int64_t request, int32_t target_mhz, double weight);
+ps_status ps_dvfs_retract(ps_dvfs* d, int64_t request);
+ps_status ps_dvfs_tick(ps_dvfs* d, int32_t* mhz, int32_t* changed);
+ps_status ps_dvfs_start(ps_dvfs* d, int32_t period_ms);
+ps_status ps_dvfs_stop(ps_dvfs* d);
+
+/* PSOpt per demand-response epoch (§IV-C "Joint formulation", eq. dual;
+ * App. B.1 eqs. lagrangian, kkt-f, dcap-df; §IV-C eq. rank). For each
+ * stage-class group i with k GPUs at frequency f (MHz):
+ *   capacity C(f) = c k^nu (1 - gamma + gamma f / f_max)  (eq. dcap-df slope)
+ *   power    k (c2 f^3 + c1 f + c0)                         (§IV-C)
+ *   impact   I(C) = (1/lam) int_C^C0 p(l) (l - C) dl, l ~ Normal(lam, sigma),
+ *            C0 = C(f_max)                                  (§IV-B)
+ * minimise sum_i w_i I_i + dt sum_i k_i P_i subject to sum_i k_i P_i <= p_max
+ * and I_i <= delta_i, f_min <= f_i <= f_max, GPU counts given. The relaxation
+ * is convex; the solver meets its KKT conditions directly: per group the
+ * frequency stationarity of eq. kkt-f by bisection (raised to the lowest
+ * frequency meeting the impact bound, whose multiplier eta follows), the
+ * power-cap multiplier mu by bisection. out[i]: the relaxed optimum f, eta,
+ * the impact, the ranking key of eq. rank (impact per watt reclaimed), and
+ * f_step: the projection onto the ladder (rounded up, then lowered one step
+ * at a time in ascending rank, the degradation ordering, while the cap is
+ * exceeded and the bound allows). PS_E_CAPACITY when no admissible
+ * frequencies meet the cap (out then holds the minimum-power point: the
+ * caller consolidates GPUs or sheds load). Host only, microseconds. */
+typedef struct {
+  double w, delta;   /* class weight, impact bound                      */
+  double k, nu;      /* GPUs, multi-GPU scaling exponent                */
+  double c, gamma;   /* per-GPU capacity at f_max (req/s), compute-bound fraction */
+  double lam, sigma; /* arrival rate: mean and standard deviation       */
+  double c2, c1, c0; /* per-GPU power model, watts with f in MHz        */
+} ps_psopt_group;
+typedef struct {
+  double f, eta, impact, rank;
+  int32_t f_step;
+} ps_psopt_result;
+ps_status ps_psopt_solve(const ps_psopt_group* groups, int32_t n, double p_max, double f_min, double f_max,
+                         double dt, const int32_t* ladder_mhz, int32_t n_ladder, ps_psopt_result* out, double* mu,
+                         double* power_relaxed, double* power_projected);
+
 /* ------------------------------------------------------------------ layer */
 ps_status ps_layer_create(const ps_layer_cfg* cfg, ps_layer** out);
 ps_status ps_layer_destroy(ps_layer* layer);

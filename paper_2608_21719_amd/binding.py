@@ -48,6 +48,18 @@ class SchedCfg(ctypes.Structure):
     _fields_ = [("window", c_int32), ("cs_initial", c_int32), ("cs_min", c_int32), ("cs_max", c_int32)]
 
 
+class PsoptGroup(ctypes.Structure):
+    _fields_ = [(n, c_double) for n in ("w", "delta", "k", "nu", "c", "gamma", "lam", "sigma", "c2", "c1", "c0")]
+
+
+class PsoptResult(ctypes.Structure):
+    _fields_ = [("f", c_double), ("eta", c_double), ("impact", c_double), ("rank", c_double), ("f_step", c_int32)]
+
+
+DVFS_LOCK_FN = ctypes.CFUNCTYPE(c_int32, c_void_p, c_int32)
+DVFS_LIMIT_FN = ctypes.CFUNCTYPE(c_int32, c_void_p, c_int32)
+
+
 class LayerW(ctypes.Structure):
     _fields_ = [("attn_norm", c_void_p), ("w_qkv", c_void_p), ("w_o", c_void_p), ("ffn_norm", c_void_p),
                 ("w_gate_up", c_void_p), ("w_down", c_void_p)]
@@ -102,6 +114,16 @@ _SIGS = {
     "ps_sched_admit": (_I, [_P, _I, _IP]),
     "ps_sched_reserve_step": (_I, [_P, _I, _IP, _IP, _IP, _I, _IP]),
     "ps_sched_finish": (_I, [_P, _I, _I]),
+    "ps_dvfs_create": (_I, [POINTER(c_int32), _I, c_double, c_double, _I, _I, DVFS_LOCK_FN, DVFS_LIMIT_FN, _P,
+                            POINTER(c_void_p)]),
+    "ps_dvfs_destroy": (_I, [_P]),
+    "ps_dvfs_vote": (_I, [_P, ctypes.c_int64, _I, c_double]),
+    "ps_dvfs_retract": (_I, [_P, ctypes.c_int64]),
+    "ps_dvfs_tick": (_I, [_P, _IP, _IP]),
+    "ps_dvfs_start": (_I, [_P, _I]),
+    "ps_dvfs_stop": (_I, [_P]),
+    "ps_psopt_solve": (_I, [POINTER(PsoptGroup), _I, c_double, c_double, c_double, c_double, POINTER(c_int32), _I,
+                            POINTER(PsoptResult), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
     "ps_layer_create": (_I, [POINTER(LayerCfg), POINTER(c_void_p)]),
     "ps_layer_destroy": (_I, [_P]),
     "ps_workspace_bytes": (c_size_t, [POINTER(LayerCfg), _I, _I, _I]),
@@ -340,6 +362,64 @@ class Sched:
 
     def finish(self, seq: int, stage_tokens: int):
         check(lib.ps_sched_finish(self.h, seq, stage_tokens))
+
+
+class Dvfs:
+    """Vote-commit DVFS daemon; lock(mhz) and limit(watts) are Python
+    callables (the actuators), called from the ticking thread."""
+
+    def __init__(self, ladder, under_weight, over_weight, power_limit_w, initial_mhz, lock=None, limit=None):
+        self._lock = DVFS_LOCK_FN(lambda ctx, mhz: int(lock(mhz) or 0) if lock else 0)
+        self._limit = DVFS_LIMIT_FN(lambda ctx, w: int(limit(w) or 0) if limit else 0)
+        arr = (c_int32 * len(ladder))(*ladder)
+        h = c_void_p()
+        check(lib.ps_dvfs_create(arr, len(ladder), under_weight, over_weight, power_limit_w, initial_mhz, self._lock,
+                                 self._limit, None, ctypes.byref(h)))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            check(lib.ps_dvfs_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def vote(self, request: int, target_mhz: int, weight: float):
+        check(lib.ps_dvfs_vote(self.h, request, target_mhz, weight))
+
+    def retract(self, request: int):
+        check(lib.ps_dvfs_retract(self.h, request))
+
+    def tick(self):
+        f, ch = c_int32(), c_int32()
+        check(lib.ps_dvfs_tick(self.h, ctypes.byref(f), ctypes.byref(ch)))
+        return f.value, bool(ch.value)
+
+    def start(self, period_ms: int):
+        check(lib.ps_dvfs_start(self.h, period_ms))
+
+    def stop(self):
+        check(lib.ps_dvfs_stop(self.h))
+
+
+def psopt_solve(groups, p_max, f_min, f_max, ladder, dt=0.0):
+    """groups: list of dicts with the PsoptGroup fields. Returns (results,
+    mu, relaxed power, projected power, status) without raising on PS_E_CAPACITY."""
+    n = len(groups)
+    g = (PsoptGroup * n)(*[PsoptGroup(*[float(x[f]) for f, _ in PsoptGroup._fields_]) for x in groups])
+    out = (PsoptResult * n)()
+    lad = (c_int32 * len(ladder))(*ladder)
+    mu, pr, pp = c_double(), c_double(), c_double()
+    rc = lib.ps_psopt_solve(g, n, p_max, f_min, f_max, dt, lad, len(ladder), out, ctypes.byref(mu), ctypes.byref(pr),
+                            ctypes.byref(pp))
+    if rc not in (PS_OK, PS_E_CAPACITY):
+        check(rc)
+    res = [{"f": r.f, "eta": r.eta, "impact": r.impact, "rank": r.rank, "f_step": r.f_step} for r in out]
+    return res, mu.value, pr.value, pp.value, rc
 
 
 class Layer:

@@ -16,6 +16,7 @@
 
 #include "../../include/ps.h"
 #include "admission.h"
+#include "control.h"
 #include "common.h"
 #include "kv_pool.h"
 #include "launch.h"
@@ -739,6 +740,84 @@ extern "C" ps_status ps_sched_finish(ps_sched* s, int32_t seq, int32_t stage_tok
   PS_TRY CHECK_SCHED(s);
   std::string e;
   if (int rc = s->adm.finish(seq, stage_tokens, e)) return fail(rc, e);
+  return PS_OK;
+  PS_CATCH
+}
+
+// ------------------------------------------------------ frequency control
+struct ps_dvfs {
+  Dvfs d;
+  template <typename... A>
+  explicit ps_dvfs(A&&... a) : d(std::forward<A>(a)...) {}
+};
+
+extern "C" ps_status ps_dvfs_create(const int32_t* ladder, int32_t n, double under_w, double over_w, int32_t limit_w,
+                                    int32_t f0, ps_dvfs_lock_fn lock, ps_dvfs_limit_fn limit, void* ctx,
+                                    ps_dvfs** out) {
+  PS_TRY
+  if (!ladder || n <= 0 || !out) return fail(PS_E_INVALID, "bad ladder or out");
+  for (int i = 1; i < n; ++i)
+    if (ladder[i] <= ladder[i - 1]) return fail(PS_E_INVALID, "ladder must increase strictly");
+  if (!(under_w >= 0) || !(over_w >= 0)) return fail(PS_E_INVALID, "negative penalty weight");
+  *out = new ps_dvfs(std::vector<int32_t>(ladder, ladder + n), under_w, over_w, limit_w, f0, lock, limit, ctx);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_dvfs_destroy(ps_dvfs* d) {
+  PS_TRY
+  delete d;
+  return PS_OK;
+  PS_CATCH
+}
+#define CHECK_DVFS(d) \
+  if (!(d)) return fail(PS_E_INVALID, "null dvfs handle");
+extern "C" ps_status ps_dvfs_vote(ps_dvfs* d, int64_t r, int32_t target, double weight) {
+  PS_TRY CHECK_DVFS(d);
+  if (!(weight >= 0)) return fail(PS_E_INVALID, "negative vote weight");
+  d->d.vote(r, target, weight);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_dvfs_retract(ps_dvfs* d, int64_t r) {
+  PS_TRY CHECK_DVFS(d);
+  d->d.retract(r);
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_dvfs_tick(ps_dvfs* d, int32_t* mhz, int32_t* changed) {
+  PS_TRY CHECK_DVFS(d);
+  if (int32_t rc = d->d.tick(mhz, changed)) return fail(PS_E_HIP, "actuator returned " + std::to_string(rc));
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_dvfs_start(ps_dvfs* d, int32_t period_ms) {
+  PS_TRY CHECK_DVFS(d);
+  if (period_ms <= 0) return fail(PS_E_INVALID, "period must be positive");
+  if (!d->d.start(period_ms)) return fail(PS_E_INVALID, "daemon already running");
+  return PS_OK;
+  PS_CATCH
+}
+extern "C" ps_status ps_dvfs_stop(ps_dvfs* d) {
+  PS_TRY CHECK_DVFS(d);
+  d->d.stop();
+  return PS_OK;
+  PS_CATCH
+}
+
+extern "C" ps_status ps_psopt_solve(const ps_psopt_group* g, int32_t n, double p_max, double f_min, double f_max,
+                                    double dt, const int32_t* ladder, int32_t n_ladder, ps_psopt_result* out,
+                                    double* mu, double* p_relaxed, double* p_projected) {
+  PS_TRY
+  if (!g || n <= 0 || !out || !ladder || n_ladder <= 0) return fail(PS_E_INVALID, "bad arguments");
+  if (!(f_min > 0) || !(f_max > f_min) || !(p_max > 0) || !(dt >= 0)) return fail(PS_E_INVALID, "bad range");
+  for (int i = 1; i < n_ladder; ++i)
+    if (ladder[i] <= ladder[i - 1]) return fail(PS_E_INVALID, "ladder must increase strictly");
+  for (int i = 0; i < n; ++i)
+    if (!(g[i].k > 0) || !(g[i].c > 0) || !(g[i].gamma >= 0 && g[i].gamma <= 1) || !(g[i].lam > 0) ||
+        !(g[i].sigma > 0) || !(g[i].delta >= 0) || !(g[i].w >= 0) || !(g[i].c2 >= 0) || !(g[i].c1 >= 0))
+      return fail(PS_E_INVALID, "bad group " + std::to_string(i));
+  if (int rc = psopt_solve(g, n, p_max, f_min, f_max, dt, ladder, n_ladder, out, mu, p_relaxed, p_projected))
+    return fail(rc, "the power cap is not reachable at the frequencies the impact bounds allow");
   return PS_OK;
   PS_CATCH
 }
