@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "decode tok/s & HBM GB/s; prefill tok/s & MFMA util (8B-shaped layer)"
+TEL = None  # telemetry.Telemetry, set in main: GPU clock and power of each timed leg
 
 
 def log(*a):
@@ -107,6 +108,7 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
         step()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
+    tel_step = observe(step)
     tokens = n * T
 
     # dominant kernel: gate_up GEMM + SwiGLU epilogue, same launch path as the layer
@@ -114,8 +116,9 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
     hn = randn(torch, gen, (M, K))
     m = torch.empty((M, sh.ffn), dtype=torch.bfloat16, device="cuda")
     timer = EventTimer(torch)
-    g_ms = timer(lambda: B.op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_SWIGLU, M, N, K, hn, tw["w_gate_up"], None, m),
-                 iters=max(3, steps))
+    gate_up = lambda: B.op_gemm(B.PS_BF16, 0, B.PS_BF16, B.PS_EPI_SWIGLU, M, N, K, hn, tw["w_gate_up"], None, m)  # noqa: E731
+    g_ms = timer(gate_up, iters=max(50, steps))
+    tel_gemm = observe(gate_up)
     flops = 2.0 * M * N * K
     gemm_tflops = flops / (g_ms * 1e-3) / 1e12
     total_gemm = A.gemm_flops(tokens, sh.hidden, sh.d_q, sh.d_kv, sh.ffn)
@@ -124,14 +127,15 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
     qa = randn(torch, gen, (tokens, sh.n_q, sh.head_dim))
     oa = torch.empty((tokens, sh.d_q), dtype=torch.bfloat16, device="cuda")
     a_ms = timer(lambda: B.op_attention(kv, 0, seqs, [T] * n, qa, oa, ws), iters=max(5, steps))
+    traffic = measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
     res = {
         "tok_s": tokens / (ms * 1e-3), "ms_per_step": ms,
         "layer_tflops": (total_gemm + attn) / (ms * 1e-3) / 1e12,
-        "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K},
+        "telemetry": tel_step,
+        "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K, "telemetry": tel_gemm},
         "attention": {"ms": a_ms, "tflops": attn / (a_ms * 1e-3) / 1e12},
-        "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s",
-                               measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
-                               ).as_dict(),
+        "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s", traffic,
+                               roofline_extra("mfma", gemm_tflops, tel_gemm, traffic)).as_dict(),
     }
     del pool, ws, tw, x, out, hn, m, qa, oa
     return res
@@ -185,19 +189,23 @@ def bench_decode(torch, B, A, wl, steps, warmup):
     aws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
     timer = EventTimer(torch)
     B.op_decode_plan(kv, seqs, aws)
-    a_ms = timer(lambda: B.op_decode_run(kv, 0, q, o, aws), iters=max(20, steps))
+    attn = lambda: B.op_decode_run(kv, 0, q, o, aws)  # noqa: E731
+    a_ms = timer(attn, iters=max(200, steps))
+    tel_attn = observe(attn)
     lens = [kv.seq_len(s) for s in seqs]
     a_bytes = A.decode_attention_bytes([L + 1 for L in lens], sh.n_kv, sh.head_dim, 2)
     a_gbs = a_bytes / (a_ms * 1e-3) / 1e9
+    tel_step = observe(lambda: layer.decode_step(w, kv, 0, B.PS_PHASE_ANSWER, seqs, x, out, ws))  # no commit
+    traffic = measured_traffic("decode_attention_b64", "paper_2608_21719_amd/csrc/k_attn_decode.hip")
     res = {
         "tok_s": nb / (ms * 1e-3), "ms_per_step": ms, "batch": nb,
         "ctx_mean": sum(ctx) / nb, "steps": steps,
         "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
         "step_bytes": kv_bytes + w_bytes,
-        "attention": {"us": a_ms * 1e3, "gbs": a_gbs, "bytes": a_bytes},
-        "roofline": A.Roofline("hbm", a_gbs, A.HBM_PEAK_GBS, "GB/s",
-                               measured_traffic("decode_attention_b64", "paper_2608_21719_amd/csrc/k_attn_decode.hip")
-                               ).as_dict(),
+        "telemetry": tel_step,
+        "attention": {"us": a_ms * 1e3, "gbs": a_gbs, "bytes": a_bytes, "telemetry": tel_attn},
+        "roofline": A.Roofline("hbm", a_gbs, A.HBM_PEAK_GBS, "GB/s", traffic,
+                               roofline_extra("hbm", a_gbs, tel_attn, traffic)).as_dict(),
     }
     del pool, ws, tw, x, out, aws
     return res
@@ -241,6 +249,7 @@ def bench_think(torch, B, A, wl, steps, warmup):
         step()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
+    tel_step = observe(lambda: layer.decode_step(w, kv, 0, B.PS_PHASE_THINK, seqs, x, out, ws))  # no commit
     kv_bytes = sum(A.decode_attention_bytes([L + i + 1 for L in lens0], sh.n_kv, sh.head_dim, 2)
                    for i in range(steps)) / steps
     w_bytes = A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2)
@@ -261,16 +270,17 @@ def bench_think(torch, B, A, wl, steps, warmup):
     def mixed():
         layer.mixed_step(w, kv, 0, new, [chunk] * nc, seqs, xm, om, ws)
 
-    m_ms = timer(mixed, iters=max(5, steps // 2))
+    m_ms = timer(mixed, iters=max(40, steps))
+    tel_mixed = observe(mixed)
     rows = nc * chunk + nb
     m_flops = A.gemm_flops(rows, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) + \
         A.prefill_attention_flops([chunk] * nc, sh.n_q, sh.head_dim)
     res = {
         "tok_s": nb / (ms * 1e-3), "ms_per_step": ms, "batch": nb, "ctx_mean": sum(ctx) / nb,
-        "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
+        "hbm_gbs": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9, "telemetry": tel_step,
         "attention": {"us": a_ms * 1e3, "gbs": a_bytes / (a_ms * 1e-3) / 1e9, "bytes": a_bytes},
         "mixed_step": {"ms": m_ms, "rows": rows, "tok_s": rows / (m_ms * 1e-3),
-                       "tflops": m_flops / (m_ms * 1e-3) / 1e12},
+                       "tflops": m_flops / (m_ms * 1e-3) / 1e12, "telemetry": tel_mixed},
     }
     del pool, ws, tw, x, out, xm, om
     return res
@@ -331,6 +341,7 @@ def bench_model70b(torch, B, A, wl, steps, warmup):
         dstep(warmup + i)
     torch.cuda.synchronize()
     d_ms = (time.perf_counter() - t0) * 1e3 / steps
+    tel_dec = observe(lambda: model.decode_step(kv, B.PS_PHASE_ANSWER, seqs, tok[0], tok[1], ws), seconds=2.0)
     kv_bytes = L * sum(A.decode_attention_bytes([x + i + 1 for x in lens0], sh.n_kv, sh.head_dim, 2)
                        for i in range(steps)) / steps
     w_bytes = L * A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2) + V * sh.hidden * 2
@@ -354,19 +365,94 @@ def bench_model70b(torch, B, A, wl, steps, warmup):
         pstep()
     torch.cuda.synchronize()
     p_ms = (time.perf_counter() - t0) * 1e3 / psteps
+    tel_pre = observe(pstep, seconds=3.0)
     p_flops = L * (A.gemm_flops(npf * tp, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) +
                    A.prefill_attention_flops([tp] * npf, sh.n_q, sh.head_dim)) + 2.0 * npf * V * sh.hidden
     res = {
         "decode": {"tok_s": nb / (d_ms * 1e-3), "ms_per_step": d_ms, "batch": nb, "ctx": ctx,
-                   "hbm_gbs": (kv_bytes + w_bytes) / (d_ms * 1e-3) / 1e9, "step_bytes": kv_bytes + w_bytes},
+                   "hbm_gbs": (kv_bytes + w_bytes) / (d_ms * 1e-3) / 1e9, "step_bytes": kv_bytes + w_bytes,
+                   "telemetry": tel_dec},
         "prefill": {"tok_s": npf * tp / (p_ms * 1e-3), "ms_per_step": p_ms,
-                    "tflops": p_flops / (p_ms * 1e-3) / 1e12},
+                    "tflops": p_flops / (p_ms * 1e-3) / 1e12, "telemetry": tel_pre},
         "hbm_resident_gb": (sum(t.numel() for tw in tws for t in tw.values()) + 2 * V * sh.hidden + pool.numel()) * 2
         / 1e9,
         "fill_s": fill_s,
     }
     del pool, ws, tws, embed, lm_head
     return res
+
+
+def phase_sweep(torch, B, A, wl):
+    """Phase asymmetry on this GPU (the paper's Observation 2, along the
+    batch axis: the clock cannot be set from an unprivileged process here).
+    For the 8B-shaped layer: prefill of n x 2048 tokens and decode of batch
+    B at context 2048, each timed, then replayed under telemetry for the
+    clock it settles at, socket power and energy per token; gamma per App.
+    B.2 eq. gamma from the step's algorithmic FLOPs and bytes against the
+    MI355X ridge (2.5 PFLOP/s over 8 TB/s)."""
+    sh = wl.shape
+    gen = torch.Generator(device="cuda").manual_seed(2024)
+    cfg = B.make_cfg(sh)
+    tw, w = make_layer_weights(torch, B, sh, gen)
+    layer = B.Layer(cfg)
+    ridge = A.ridge_point(A.BF16_DENSE_PEAK_TFLOPS * 1e12, A.HBM_PEAK_GBS * 1e9)
+    wbytes = A.weight_bytes(sh.hidden, sh.d_q, sh.d_kv, sh.ffn, 2)
+    timer = EventTimer(torch)
+    rows = []
+
+    def record(phase, batch, tokens, ms, flops, nbytes, tel):
+        # sampled socket power (the driver's energy counter reads about 1.3x
+        # the sampled power under load on this platform while agreeing at
+        # idle, so its scale is not used)
+        pw = ((tel or {}).get("power_w") or {}).get("median")
+        clk = ((tel or {}).get("gfxclk_mhz") or {}).get("median")
+        ai = flops / nbytes
+        rows.append({"phase": phase, "batch": batch, "tokens_per_step": tokens, "ms": ms,
+                     "tok_s": tokens / (ms * 1e-3), "tflops": flops / (ms * 1e-3) / 1e12,
+                     "hbm_gbs": nbytes / (ms * 1e-3) / 1e9, "ai_flop_per_byte": ai,
+                     "gamma": A.gamma(ai, ridge), "gfxclk_mhz": clk, "power_w": pw,
+                     "joule_per_token": (pw * ms * 1e-3 / tokens) if pw else None})
+        log(f"sweep {phase} B={batch}: {tokens / (ms * 1e-3):.0f} tok/s, clk {clk} MHz, power {pw} W")
+
+    ctx = 2048
+    for nb in (1, 4, 16, 64, 256):
+        pages = (ctx + 16) // 16
+        pool = torch.empty(B.KV.pool_bytes(cfg, 1, nb * pages + 8), dtype=torch.uint8, device="cuda")
+        kv = B.KV(cfg, 1, nb * pages + 8, nb, pages, pool, seed=77)
+        seqs = [kv.open() for _ in range(nb)]
+        for s_ in seqs:
+            kv.alloc(s_, ctx + 1)
+            kv.commit([s_], [ctx])
+        ws = torch.empty(B.Layer.workspace_bytes(cfg, nb, nb, pages), dtype=torch.uint8, device="cuda")
+        x = randn(torch, gen, (nb, sh.hidden))
+        out = torch.empty_like(x)
+        step = lambda: layer.decode_step(w, kv, 0, B.PS_PHASE_ANSWER, seqs, x, out, ws)  # noqa: E731
+        ms = timer(step, iters=50)
+        flops = A.gemm_flops(nb, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) + \
+            A.decode_attention_flops([ctx + 1] * nb, sh.n_q, sh.head_dim)
+        nbytes = wbytes + A.decode_attention_bytes([ctx + 1] * nb, sh.n_kv, sh.head_dim, 2)
+        record("decode", nb, nb, ms, flops, nbytes, observe(step, seconds=1.2))
+        del pool, ws
+    T = 2048
+    for n in (1, 4, 8):
+        pages = T // 16
+        pool = torch.empty(B.KV.pool_bytes(cfg, 1, n * pages + 8), dtype=torch.uint8, device="cuda")
+        kv = B.KV(cfg, 1, n * pages + 8, n, pages, pool, seed=78)
+        seqs = [kv.open() for _ in range(n)]
+        for s_ in seqs:
+            kv.alloc(s_, T)
+        ws = torch.empty(B.Layer.workspace_bytes(cfg, n * T, n, pages), dtype=torch.uint8, device="cuda")
+        x = randn(torch, gen, (n * T, sh.hidden))
+        out = torch.empty_like(x)
+        step = lambda: layer.prefill(w, kv, 0, seqs, [T] * n, x, out, ws)  # noqa: E731
+        ms = timer(step, iters=10)
+        flops = A.gemm_flops(n * T, sh.hidden, sh.d_q, sh.d_kv, sh.ffn) + \
+            A.prefill_attention_flops([T] * n, sh.n_q, sh.head_dim)
+        nbytes = wbytes + 2 * n * T * sh.hidden * 2 + n * T * 2 * sh.d_kv * 2
+        record("prefill", n, n * T, ms, flops, nbytes, observe(step, seconds=1.2))
+        del pool, ws
+    del tw
+    return rows
 
 
 def cpu_baseline(wl, n_tokens, budget_s=10.0):
@@ -385,10 +471,59 @@ def cpu_baseline(wl, n_tokens, budget_s=10.0):
         O.layer_sequence(w, wl.shape, x[done * n_tokens:(done + 1) * n_tokens])
         dt += time.perf_counter() - t0
         done += 1
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    model = ""
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": done * n_tokens / dt, "unit": "tok/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} of the {wl.prefill_seqs} prompts x {n_tokens} tokens of the prefill workload, "
-                      f"fp64 numpy, {dt:.1f} s"}
+                      f"fp64 numpy, {dt:.1f} s",
+            "affinity_cores": len(os.sched_getaffinity(0)), "blas_threads": threads,
+            "blas": ", ".join(sorted({f"{p.get('internal_api')} {p.get('version')}" for p in blas})),
+            "cpu_model": model}
+
+
+def roofline_extra(bound, achieved, tel, traffic):
+    """Context for a roofline line: where the peak comes from, the peak this
+    device derives from its own properties, the clock the kernel actually ran
+    at (the MFMA peak scales with it; MI355X under a full MFMA load runs at its
+    power cap below the peak clock) and where the traffic figure comes from."""
+    from paper_2608_21719_amd import accounting as A
+    ex = {"peak_source": "MI355X published dense bf16 MFMA peak" if bound == "mfma" else
+          "MI355X published HBM3E bandwidth"}
+    if DEVICE:
+        ex["device"] = {k: DEVICE[k] for k in ("compute_units", "clock_khz", "arch")}
+        if bound == "mfma":
+            ex["peak_derived"] = A.bf16_peak_tflops(DEVICE["compute_units"], DEVICE["clock_khz"] / 1e3)
+    clk = (tel or {}).get("gfxclk_mhz") or {}
+    if clk:
+        ex["gfxclk_mhz_median"] = clk["median"]
+        if bound == "mfma" and DEVICE:
+            p = A.bf16_peak_tflops(DEVICE["compute_units"], clk["median"])
+            ex["peak_at_measured_clock"] = p
+            ex["frac_at_measured_clock"] = achieved / p
+    pw = (tel or {}).get("power_w") or {}
+    if pw:
+        ex["power_w_median"] = pw["median"]
+    ex["traffic_source"] = ("stored: profiles/traffic.json, two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) "
+                            "scaled by a known-size copy, taken on this kernel's current source"
+                            if traffic is not None else "none: no counters taken on this kernel's current source")
+    return ex
+
+
+DEVICE = None  # ps_get_device_info of cuda:0, set in main
+
+
+def observe(run, seconds=1.5):
+    """GPU clock and power while the leg's work repeats (after its timed region)."""
+    import torch
+    return TEL.observe(run, torch.cuda.synchronize, seconds=seconds)
 
 
 def measured_traffic(kernel_key, source_file):
@@ -417,6 +552,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--no-model70b", action="store_true", help="skip the 80-layer 70B-shaped model")
+    ap.add_argument("--phase-sweep", action="store_true",
+                    help="also measure throughput, clock, power and energy per token across phases and batch sizes")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one 1 GiB device copy first (known bytes, to scale rocprof counters)")
     a = ap.parse_args()
@@ -435,6 +572,10 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    global TEL, DEVICE
+    from paper_2608_21719_amd.telemetry import Telemetry
+    TEL = Telemetry(0)
+    DEVICE = B.device_info(0)
     if a.calib_copy:
         # int32 -> fp32 conversion copy: reads exactly 1 GiB, writes exactly 1 GiB
         src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
@@ -470,6 +611,11 @@ def main():
         log(f"model70b: decode {m70['decode']['tok_s']:.0f} tok/s ({m70['decode']['ms_per_step']:.1f} ms/step, "
             f"{m70['decode']['hbm_gbs']:.0f} GB/s), prefill {m70['prefill']['tok_s']:.0f} tok/s")
         torch.cuda.empty_cache()
+    sweep = None
+    if a.phase_sweep:
+        log("phase sweep: 8B-shaped layer, decode B in {1..256} at context 2048, prefill n x 2048")
+        sweep = phase_sweep(torch, B, A, CONFIGS["llama8b_decode"])
+        torch.cuda.empty_cache()
     cpu = None
     if not a.no_cpu_baseline:
         log("cpu baseline: fp64 oracle on the host")
@@ -482,12 +628,17 @@ def main():
                                "heads, head_dim 128, SwiGLU 14336), bf16 weights/activations, fp32 accumulate",
                    "global_batch": 8, "seq_len": 2048, "parallelism": "single GPU"},
         "roofline": pre["roofline"],
+        "device": dict(DEVICE, bf16_peak_derived_tflops=A.bf16_peak_tflops(DEVICE["compute_units"],
+                                                                            DEVICE["clock_khz"] / 1e3),
+                       telemetry=TEL.static_info()),
         "prefill": {k: v for k, v in pre.items() if k != "roofline"},
         "decode": dec,
         "think": think,
         "model70b": m70,
         "cpu_baseline": cpu,
     }
+    if sweep is not None:
+        line["phase_sweep"] = sweep
     print(json.dumps(line), flush=True)
 
 

@@ -6,4 +6,4 @@ fails loudly when the library is missing. ``accounting`` holds the
 algorithmic FLOP/byte counts used to express timings as roofline fractions.
 Importing the package does not load the library.
 """
-__version__ = "0.1.0"
+__version__ = "0.2.0"

@@ -17,6 +17,16 @@ BF16_DENSE_PEAK_TFLOPS = 2500.0
 FP32_VECTOR_PEAK_TFLOPS = 157.3
 
 
+# dense bf16 MFMA FLOPs per compute unit per clock on gfx950 (four SIMDs, each
+# one 32x32x16 bf16 MFMA = 32768 FLOPs per 32 cycles)
+BF16_FLOP_PER_CU_CLOCK = 4096
+
+
+def bf16_peak_tflops(compute_units: int, clock_mhz: float) -> float:
+    """Dense bf16 MFMA peak at a given engine clock (TFLOP/s)."""
+    return compute_units * BF16_FLOP_PER_CU_CLOCK * clock_mhz * 1e6 / 1e12
+
+
 def layer_params(d: int, d_q: int, d_kv: int, ffn: int, gated: bool = True) -> int:
     """Weight count of the four projections (norm gains excluded)."""
     return d * (d_q + 2 * d_kv) + d_q * d + (3 if gated else 2) * d * ffn
@@ -104,7 +114,10 @@ class Roofline:
     peak: float
     unit: str
     traffic: object = None
+    extra: dict = None
 
     def as_dict(self) -> dict:
-        return {"bound": self.bound, "achieved": self.achieved, "peak": self.peak,
-                "unit": self.unit, "frac": self.achieved / self.peak, "traffic": self.traffic}
+        d = {"bound": self.bound, "achieved": self.achieved, "peak": self.peak,
+             "unit": self.unit, "frac": self.achieved / self.peak, "traffic": self.traffic}
+        d.update(self.extra or {})
+        return d
