@@ -53,6 +53,12 @@ template <> __device__ __forceinline__ void st_elt<bf16_t>(bf16_t* p, long i, fl
 __device__ __forceinline__ void load_lds16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
 }
+// The same with a wave-uniform byte offset in the scalar offset operand: a
+// per-stage step added there costs no vector address arithmetic.
+__device__ __forceinline__ void load_lds16_buf_so(__amdgpu_buffer_rsrc_t r, uint32_t voffset, uint32_t soffset,
+                                                  bf16_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, soffset, 0, 0);
+}
 // The same with the non-temporal hint (cache policy bit 1), for data read
 // exactly once per call (decode weight streams).
 __device__ __forceinline__ void load_lds16_buf_nt(__amdgpu_buffer_rsrc_t r, uint32_t voffset, bf16_t* lds) {
@@ -176,13 +182,14 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(A + (long)m0 * K, (uint32_t)min(M - m0, BM) * K * 2);
   const __amdgpu_buffer_rsrc_t rW =
       buffer_rsrc(W + (long)(n0 >> 6) * (K / 64) * kWTileElts, (uint32_t)(BN / 64) * (K / 64) * kWTileElts * 2);
-  // DMA instruction l (0..LOADS-1) of stage s into slot s & 1
-  auto dma = [&](int s, int l) __attribute__((always_inline)) {
-    bf16_t* st = smem + (s & 1) * STAGE;
+  // DMA instruction l (0..LOADS-1) of stage s into slot dslot (= s & 1);
+  // the stage's step rides in the scalar offset
+  auto dma = [&](int s, int dslot, int l) __attribute__((always_inline)) {
+    bf16_t* st = smem + dslot * STAGE;
     if (l < A_LOADS)
-      load_lds16_buf(rA, aoff[l] + s * BK * 2, st + (wave * A_LOADS + l) * RPL * BK);
+      load_lds16_buf_so(rA, aoff[l], s * BK * 2, st + (wave * A_LOADS + l) * RPL * BK);
     else
-      load_lds16_buf(rW, boff[l - A_LOADS] + s * kWTileElts * 2, st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
+      load_lds16_buf_so(rW, boff[l - A_LOADS], s * kWTileElts * 2, st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
   };
 
   // 32x32x16 operands: lane (h, r) holds row r of a 32-row block, k 8h..8h+7
@@ -216,8 +223,13 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
 
   const int T = K / BK;
   // stage st; `full` = st + 2 < T (every condition below holds)
-  auto stage = [&](int st, bool full) __attribute__((always_inline)) {
-    const int slot = st & 1;
+  // slotc: std::integral_constant<int, st & 1> where the caller knows the
+  // parity (LDS slot addresses then fold into instruction offsets), else an
+  // int and the slot is computed
+  auto stage = [&](int st, bool full, auto slotc) __attribute__((always_inline)) {
+    int slot;
+    if constexpr (std::is_same_v<decltype(slotc), int>) slot = st & 1;
+    else slot = decltype(slotc)::value;
     const bool more = full || st + 1 < T;
     const bool dma_next = st > 0 && st + 1 < T;  // rest of stage st+1 (stage 1 comes whole with the prologue)
     const bool dma_far = full || st + 2 < T;     // first part of stage st+2
@@ -236,7 +248,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
           if (rd) read_frag(rslot, (sl + 1) & 3, q);
         }
         if constexpr (q >= DMA_AT && (q - DMA_AT) % DMA_EVERY == 0 && (q - DMA_AT) / DMA_EVERY < DN) {
-          if (dd) dma(ds, DB + (q - DMA_AT) / DMA_EVERY);
+          if (dd) dma(ds, sl == 3 ? slot : slot ^ 1, DB + (q - DMA_AT) / DMA_EVERY);
         }
       });
       if (full) {
@@ -265,10 +277,10 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   // prologue: stages 0 and 1 whole, stage 0 landed everywhere, its first
   // fragments read
 #pragma unroll
-  for (int l = 0; l < LOADS; ++l) dma(0, l);
+  for (int l = 0; l < LOADS; ++l) dma(0, 0, l);
   if (T > 1) {
 #pragma unroll
-    for (int l = 0; l < LOADS; ++l) dma(1, l);
+    for (int l = 0; l < LOADS; ++l) dma(1, 1, l);
     wait_vmcnt_lgkm0<LOADS>();
   } else {
     wait_vmcnt_lgkm0<0>();
@@ -277,8 +289,14 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
 #pragma unroll
   for (int r = 0; r < 2 * Q; ++r) read_frag(0, 0, r);
   int st = 0;
-  for (; st + 2 < T; ++st) stage(st, true);
-  for (; st < T; ++st) stage(st, false);
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  for (; st + 3 < T; st += 2) {  // two stages per trip: both slots known at compile time
+    stage(st, true, S0{});
+    stage(st + 1, true, S1{});
+  }
+  if (st + 2 < T) stage(st++, true, S0{});  // st is even here
+  for (; st < T; ++st) stage(st, false, 0);
 
   // epilogue: acc[i][j][r] is C[32 i + 8 (r / 4) + 4 h + r % 4][32 j + r32]
   // of the wave tile. Each 32-row block goes through a wave-private LDS
