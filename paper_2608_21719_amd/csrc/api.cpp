@@ -223,12 +223,63 @@ struct ps_kv {
   }
 };
 
+// A second stream on the caller's device (default priority, non-blocking)
+// and the events that fork work onto it and join it back inside one call.
+// Created on first use; a handle is driven by one host thread at a time.
+struct AuxStream {
+  static constexpr int kEvents = 4;
+  int dev = -1;
+  hipStream_t s = nullptr;
+  hipEvent_t ev[kEvents] = {};
+  AuxStream() = default;
+  AuxStream(const AuxStream&) = delete;
+  AuxStream& operator=(const AuxStream&) = delete;
+  ~AuxStream() {
+    for (hipEvent_t& e : ev)
+      if (e) (void)hipEventDestroy(e);
+    if (s) (void)hipStreamDestroy(s);
+  }
+  // *out = this, ready for work forked from `caller`, or nullptr when the
+  // caller's stream is not on the current device or the stream was made
+  // for another device (the call then runs on the caller's stream alone).
+  ps_status get(hipStream_t caller, AuxStream** out) {
+    *out = nullptr;
+    int cur = 0, sdev = 0;
+    if (hipError_t e = hipGetDevice(&cur)) return hip_fail(e, "current device");
+    if (caller) {
+      if (hipError_t e = hipStreamGetDevice(caller, &sdev)) return hip_fail(e, "stream device");
+    } else {
+      sdev = cur;
+    }
+    if (sdev != cur || (dev >= 0 && dev != cur)) return PS_OK;
+    if (dev < 0) {
+      hipStream_t ns = nullptr;
+      hipEvent_t ne[kEvents] = {};
+      hipError_t e = hipStreamCreateWithFlags(&ns, hipStreamNonBlocking);
+      for (int i = 0; i < kEvents && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&ne[i], hipEventDisableTiming);
+      if (e != hipSuccess) {
+        for (hipEvent_t x : ne)
+          if (x) (void)hipEventDestroy(x);
+        if (ns) (void)hipStreamDestroy(ns);
+        return hip_fail(e, "auxiliary stream and its events");
+      }
+      s = ns;
+      for (int i = 0; i < kEvents; ++i) ev[i] = ne[i];
+      dev = cur;
+    }
+    *out = this;
+    return PS_OK;
+  }
+};
+
 struct ps_layer {
   ps_layer_cfg cfg;
+  AuxStream aux;
 };
 
 struct ps_model {
   ps_layer_cfg cfg;
+  AuxStream aux;
   int32_t n_layers = 0, vocab = 0;
   const void* embed = nullptr;
   const void* final_norm = nullptr;
@@ -518,7 +569,7 @@ std::vector<double> inv_freq(const ps_layer_cfg& c) {
 
 // Workspace carve-out for a layer call (after the metadata region).
 struct WsLayout {
-  size_t xn, qkv, qr, o, h, m, gemm, apart_o, apart_ml, total;
+  size_t xn, qkv, qr, o, h, m, gemm, gemm_b, apart_o, apart_ml, total;
 };
 
 WsLayout layout(const ps_layer_cfg& c, size_t meta_bytes, int32_t rows, int32_t n_parts_max) {
@@ -547,7 +598,21 @@ WsLayout layout(const ps_layer_cfg& c, size_t meta_bytes, int32_t rows, int32_t 
     g = std::max(g, gemm_workspace_bytes(c.dtype, gm, 2 * c.ffn, (int)d));
     g = std::max(g, gemm_workspace_bytes(c.dtype, gm, (int)d, c.ffn));
   }
+  // K-split partials of the tile-path O and down GEMMs, for any row count
+  // up to `rows` (a call's chunk rows included)
+  if (c.dtype == PS_BF16 && rows > 0) {
+    g = std::max(g, gemm_tile_partials_bound(rows, (int)d, (int)dq));
+    g = std::max(g, gemm_tile_partials_bound(rows, (int)d, c.ffn));
+  }
   L.gemm = take(g);
+  // the decode rows' O and down partials when they run on the second
+  // stream beside the chunk rows
+  size_t gb = 0;
+  if (gm > 0) {
+    gb = std::max(gb, gemm_workspace_bytes(c.dtype, gm, (int)d, (int)dq));
+    gb = std::max(gb, gemm_workspace_bytes(c.dtype, gm, (int)d, c.ffn));
+  }
+  L.gemm_b = take(gb);
   L.apart_o = take((size_t)n_parts_max * dq * 4);
   L.apart_ml = take((size_t)n_parts_max * c.n_q_heads * 2 * 4);
   L.total = off;
@@ -932,24 +997,96 @@ ps_status stage_meta(ps_kv* kv, const Meta& mt, void* ws, UploadJob* job) {
 // `up`, if given, is the call's metadata upload: the first kernel carries it
 // (every kernel that reads the metadata runs after that one).
 int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w, void* pool, const void* x_in,
-                 void* x_out, char* W, hipStream_t st, const UploadJob* up = nullptr) {
+                 void* x_out, char* W, hipStream_t st, const UploadJob* up = nullptr, AuxStream* aux = nullptr) {
   const WsLayout& wl = P.wl;
   const int d = c.hidden, dq = c.n_q_heads * c.head_dim, dkv = c.n_kv_heads * c.head_dim;
   const int dt = c.dtype, G = group_of(c), rows = P.rows;
   const SeqInfo* si = (const SeqInfo*)(W + P.o_si);
   const int32_t* bt = (const int32_t*)(W + P.o_bt);
-  void* xn = W + wl.xn;
+  char* xn = W + wl.xn;
   void* qkv = W + wl.qkv;
-  void* qr = W + wl.qr;
-  void* o = W + wl.o;
-  void* h = W + wl.h;
-  void* m = W + wl.m;
+  char* qr = W + wl.qr;
+  char* o = W + wl.o;
+  char* h = W + wl.h;
+  char* m = W + wl.m;
   void* gws = W + wl.gemm;
-  const size_t gws_bytes = wl.apart_o - wl.gemm;
+  const size_t gws_bytes = wl.gemm_b - wl.gemm;
+  void* gws_b = W + wl.gemm_b;
+  const size_t gws_b_bytes = wl.apart_o - wl.gemm_b;
   const size_t eb = elt_bytes(dt);
   const float scale = 1.0f / std::sqrt((float)c.head_dim);
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  // bf16, d a multiple of 8 up to 8192: a row fits the fused split-sum +
+  // residual + RMSNorm kernel's registers
+  const bool fused_norm = dt == PS_BF16 && d % 8 == 0 && d <= 8192;
   int bad = 0;
+
+  // O projection + residual -> h (fp32), then the FFN RMSNorm -> xn, over
+  // `n` rows from row r0. Split-K partials (a decode-sized skinny plan, or a
+  // tile launch that would leave compute units idle) are summed by the norm
+  // kernel, which also adds the residual and stores h.
+  auto o_proj = [&](int r0, int n, void* ws, size_t ws_bytes, hipStream_t s) {
+    if (n == 0) return;
+    const char* a = o + (size_t)r0 * dq * eb;
+    const char* res = (const char*)x_in + (size_t)r0 * d * eb;
+    float* hr = (float*)(h + (size_t)r0 * d * 4);
+    char* y = xn + (size_t)r0 * d * eb;
+    int S = 1;
+    if (fused_norm) {
+      S = gemm_tile_splits(n, d, dq);
+      if (S > 1) {
+        if (ws_bytes < (size_t)S * n * d * 4) bad |= 1;
+        else bad |= launch_gemm_tile_split(n, d, dq, S, a, w->w_o, (float*)ws, s);
+      } else {
+        bad |= launch_gemm_split(dt, dt, PS_F32, PS_EPI_RESIDUAL, n, d, dq, a, w->w_o, res, hr, ws, ws_bytes, s, &S);
+      }
+    } else {
+      bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, n, d, dq, a, w->w_o, res, hr, ws, ws_bytes, s);
+    }
+    if (S > 1)
+      bad |= launch_split_residual_rmsnorm(n, d, S, (const float*)ws, res, hr, w->ffn_norm, c.rms_eps, y, s);
+    else
+      bad |= launch_rmsnorm(PS_F32, dt, dt, n, d, hr, w->ffn_norm, c.rms_eps, y, s);
+  };
+  // down projection + residual (h) -> x_out over `n` rows from row r0
+  auto down_proj = [&](int r0, int n, void* ws, size_t ws_bytes, hipStream_t s) {
+    if (n == 0) return;
+    const char* a = m + (size_t)r0 * c.ffn * eb;
+    const float* hr = (const float*)(h + (size_t)r0 * d * 4);
+    char* y = (char*)x_out + (size_t)r0 * d * eb;
+    const int S = dt == PS_BF16 ? gemm_tile_splits(n, d, c.ffn) : 1;
+    if (S > 1) {
+      if (ws_bytes < (size_t)S * n * d * 4) {
+        bad |= 1;
+        return;
+      }
+      bad |= launch_gemm_tile_split(n, d, c.ffn, S, a, w->w_down, (float*)ws, s);
+      bad |= launch_split_residual(PS_F32, dt, n, d, S, (const float*)ws, hr, y, s);
+    } else {
+      bad |= launch_gemm(dt, PS_F32, dt, PS_EPI_RESIDUAL, n, d, c.ffn, a, w->w_down, hr, y, ws, ws_bytes, s);
+    }
+  };
+  auto prefill_attn = [&](hipStream_t s) {
+    if (P.fa)
+      bad |= launch_fa_prefill(G, P.n_pitems, c.n_kv_heads, qr, pool, si, bt, (const PrefillItem*)(W + P.o_pi), o,
+                               scale_log2, s);
+    else
+      bad |= launch_attn_generic(dt, 0, P.chunk_rows, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr, pool, si,
+                                 bt, o, scale, s);
+  };
+  auto decode_attn = [&](hipStream_t s) {
+    if (P.dec_mfma) {
+      const char* qd = qr + (size_t)P.chunk_rows * dq * eb;
+      char* od = o + (size_t)P.chunk_rows * dq * eb;
+      bad |= launch_decode_attn(G, P.n_ditems, c.n_kv_heads, P.n_dec, qd, pool, si + P.n_chunk, bt,
+                                (const DecodeItem*)(W + P.o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
+                                (const int32_t*)(W + P.o_pb), (const int32_t*)(W + P.o_pc), od, scale_log2, s);
+    } else {
+      bad |= launch_attn_generic(dt, P.chunk_rows, P.n_dec, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
+                                 pool, si, bt, o, scale, s);
+    }
+  };
+
   bad |= launch_rmsnorm(dt, dt, dt, rows, d, x_in, w->attn_norm, c.rms_eps, xn, st, up);
   // decode-sized QKV: RoPE + KV write sums the split-K partials itself
   // (bf16, head_dim a multiple of 8: the fused reader's vector width)
@@ -961,43 +1098,40 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
     bad |= launch_gemm(dt, 0, dt, PS_EPI_STORE, rows, dq + 2 * dkv, d, xn, w->w_qkv, nullptr, qkv, gws, gws_bytes, st);
   bad |= launch_rope_kvwrite(dt, rows, qkv, qr, pool, si, bt, (const double*)(W + P.o_fr), P.n_seqs, c.n_q_heads,
                              c.n_kv_heads, c.head_dim, st, (const float*)gws, s_qkv);
-  // attention: prefill rows on the flash kernel, decode rows on the split-K
-  // kernel, anything else (fp32, other head sizes) on the vector kernel
-  if (P.n_chunk > 0) {
-    if (P.fa)
-      bad |= launch_fa_prefill(G, P.n_pitems, c.n_kv_heads, qr, pool, si, bt, (const PrefillItem*)(W + P.o_pi), o,
-                               scale_log2, st);
-    else
-      bad |= launch_attn_generic(dt, 0, P.chunk_rows, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr, pool, si,
-                                 bt, o, scale, st);
+
+  // A mixed batch (prefill chunks + decode rows) splits after the KV write:
+  // the decode rows' attention (HBM-bound over long contexts) and their
+  // skinny O and down GEMMs run on the second stream while the chunk rows'
+  // flash attention and tile GEMMs run on the caller's; the SwiGLU GEMM
+  // takes all rows at once. The two row sets write disjoint rows of o, h,
+  // xn and x_out, and each stream has its own split-K partials.
+  const bool fork = aux && P.n_chunk > 0 && P.n_dec > 0 && P.n_dec <= 64 && P.chunk_rows > 64 && fused_norm;
+  if (!fork) {
+    if (P.n_chunk > 0) prefill_attn(st);
+    if (P.n_dec > 0) decode_attn(st);
+    o_proj(0, rows, gws, gws_bytes, st);
+    bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes,
+                       st);
+    down_proj(0, rows, gws, gws_bytes, st);
+    return bad;
   }
-  if (P.n_dec > 0) {
-    if (P.dec_mfma) {
-      const char* qd = (const char*)qr + (size_t)P.chunk_rows * dq * eb;
-      char* od = (char*)o + (size_t)P.chunk_rows * dq * eb;
-      bad |= launch_decode_attn(G, P.n_ditems, c.n_kv_heads, P.n_dec, qd, pool, si + P.n_chunk, bt,
-                                (const DecodeItem*)(W + P.o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
-                                (const int32_t*)(W + P.o_pb), (const int32_t*)(W + P.o_pc), od, scale_log2, st);
-    } else {
-      bad |= launch_attn_generic(dt, P.chunk_rows, P.n_dec, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
-                                 pool, si, bt, o, scale, st);
-    }
-  }
-  // decode-sized O projection: one kernel sums the split-K partials, adds the
-  // residual, stores h and normalises it
-  // (bf16, d a multiple of 8 up to 8192: a row fits the fused kernel's registers)
-  int s_o = 1;
-  if (dt == PS_BF16 && d % 8 == 0 && d <= 8192)
-    bad |= launch_gemm_split(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st, &s_o);
-  else
-    bad |= launch_gemm(dt, dt, PS_F32, PS_EPI_RESIDUAL, rows, d, dq, o, w->w_o, x_in, h, gws, gws_bytes, st);
-  if (s_o > 1)
-    bad |= launch_split_residual_rmsnorm(rows, d, s_o, (const float*)gws, x_in, (float*)h, w->ffn_norm, c.rms_eps, xn,
-                                         st);
-  else
-    bad |= launch_rmsnorm(PS_F32, dt, dt, rows, d, h, w->ffn_norm, c.rms_eps, xn, st);
+  const hipStream_t sb = aux->s;
+  const int cr = P.chunk_rows;
+  auto link = [&](hipStream_t from, hipStream_t to, int i) {  // `to` waits for the work enqueued on `from` so far
+    if (hipEventRecord(aux->ev[i], from) != hipSuccess || hipStreamWaitEvent(to, aux->ev[i], 0) != hipSuccess)
+      bad |= 1;
+  };
+  link(st, sb, 0);
+  decode_attn(sb);
+  o_proj(cr, P.n_dec, gws_b, gws_b_bytes, sb);
+  prefill_attn(st);
+  o_proj(0, cr, gws, gws_bytes, st);
+  link(sb, st, 1);
   bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes, st);
-  bad |= launch_gemm(dt, PS_F32, dt, PS_EPI_RESIDUAL, rows, d, c.ffn, m, w->w_down, h, x_out, gws, gws_bytes, st);
+  link(st, sb, 2);
+  down_proj(cr, P.n_dec, gws_b, gws_b_bytes, sb);
+  down_proj(0, cr, gws, gws_bytes, st);
+  link(sb, st, 3);  // joined: the call's work is on the caller's stream again
   return bad;
 }
 
@@ -1027,9 +1161,12 @@ ps_status run_layer(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, 
   P.wl = layout(c, P.mt.size(), P.rows, P.n_parts);
   if (ps_status rc = check_ws(ws, ws_bytes, P.wl.total)) return rc;
   hipStream_t st = (hipStream_t)stream;
+  AuxStream* aux = nullptr;
+  if (n_chunk > 0 && n_dec > 0)
+    if (ps_status rc = L->aux.get(st, &aux)) return rc;
   UploadJob up;
   if (ps_status rc = stage_meta(kv, P.mt, ws, &up)) return rc;
-  if (launch_layer(c, P, w, kv->layer_base(layer), x_in, x_out, (char*)ws, st, &up))
+  if (launch_layer(c, P, w, kv->layer_base(layer), x_in, x_out, (char*)ws, st, &up, aux))
     return fail(PS_E_UNSUPPORTED, "a kernel rejected its configuration");
   return last_launch_error();
 }
@@ -1092,13 +1229,16 @@ ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, cons
   const ModelWs mw = model_layout(c, M->vocab, P.wl.total, P.rows, n_out);
   if (ps_status rc = check_ws(ws, ws_bytes, mw.total)) return rc;
   hipStream_t st = (hipStream_t)stream;
+  AuxStream* aux = nullptr;
+  if (n_chunk > 0 && n_dec > 0)
+    if (ps_status rc = M->aux.get(st, &aux)) return rc;
   if (ps_status rc = upload_meta(kv, P.mt, ws, st)) return rc;
   char* W = (char*)ws;
   int bad = launch_embed(P.rows, c.hidden, M->vocab, M->embed, tokens, W + mw.xa, st);
   char* cur = W + mw.xa;
   char* nxt = W + mw.xb;
   for (int l = 0; l < M->n_layers; ++l) {
-    bad |= launch_layer(c, P, &M->layers[l], kv->layer_base(l), cur, nxt, W, st);
+    bad |= launch_layer(c, P, &M->layers[l], kv->layer_base(l), cur, nxt, W, st, nullptr, aux);
     std::swap(cur, nxt);
   }
   float* logits = logits_out ? logits_out : (float*)(W + mw.logits);

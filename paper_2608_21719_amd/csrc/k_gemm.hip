@@ -143,7 +143,7 @@ __device__ __forceinline__ int swz(int row, int ch) { return row * BK + ((ch ^ (
 template <int EPI, typename TR, typename TC>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                         const TR* __restrict__ R, TC* __restrict__ C, int M, int N,
-                                                        int K, int tiles_n, int group) {
+                                                        int K, int tiles_n, int group, int splits) {
   using namespace tile;
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
 
@@ -151,10 +151,16 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   // 8 XCDs; give each XCD a contiguous range of tiles, walked in groups of
   // `group` tile-rows across N, so that tiles sharing A and W panels meet in
   // the same L2.
+  // With splits > 1 (EPI 0, fp32 C) the grid holds every tile once per K
+  // split, split-major: split s covers stages [s T / splits, (s + 1) T /
+  // splits) and stores its partial at C + s M N.
   const int nwg = gridDim.x;
   int id = blockIdx.x;
   if ((nwg & 7) == 0) id = (id & 7) * (nwg >> 3) + (id >> 3);
-  const int tiles_m = nwg / tiles_n;
+  const int n_tiles = nwg / splits;
+  const int ks = id / n_tiles;
+  id -= ks * n_tiles;
+  const int tiles_m = n_tiles / tiles_n;
   const int group_sz = group * tiles_n;
   const int first_m = (id / group_sz) * group;
   const int gm = min(group, tiles_m - first_m);
@@ -182,14 +188,17 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(A + (long)m0 * K, (uint32_t)min(M - m0, BM) * K * 2);
   const __amdgpu_buffer_rsrc_t rW =
       buffer_rsrc(W + (long)(n0 >> 6) * (K / 64) * kWTileElts, (uint32_t)(BN / 64) * (K / 64) * kWTileElts * 2);
+  const int T_all = K / BK;
+  const int st0 = ks * T_all / splits, T = (ks + 1) * T_all / splits - st0;  // this workgroup's stages
   // DMA instruction l (0..LOADS-1) of stage s into slot dslot (= s & 1);
   // the stage's step rides in the scalar offset
   auto dma = [&](int s, int dslot, int l) __attribute__((always_inline)) {
     bf16_t* st = smem + dslot * STAGE;
     if (l < A_LOADS)
-      load_lds16_buf_so(rA, aoff[l], s * BK * 2, st + (wave * A_LOADS + l) * RPL * BK);
+      load_lds16_buf_so(rA, aoff[l], (s + st0) * BK * 2, st + (wave * A_LOADS + l) * RPL * BK);
     else
-      load_lds16_buf_so(rW, boff[l - A_LOADS], s * kWTileElts * 2, st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
+      load_lds16_buf_so(rW, boff[l - A_LOADS], (s + st0) * kWTileElts * 2,
+                        st + A_ELTS + (wave * B_LOADS + l - A_LOADS) * RPL * BK);
   };
 
   // 32x32x16 operands: lane (h, r) holds row r of a 32-row block, k 8h..8h+7
@@ -221,7 +230,6 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
     acc[q / Q][q % Q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[sl & 1][q / Q], fb[sl & 1][q % Q], acc[q / Q][q % Q], 0, 0, 0);
   };
 
-  const int T = K / BK;
   // stage st; `full` = st + 2 < T (every condition below holds)
   // slotc: std::integral_constant<int, st & 1> where the caller knows the
   // parity (LDS slot addresses then fold into instruction offsets), else an
@@ -315,6 +323,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   constexpr int LPR = OUT_COLS / V, RPP = 64 / LPR;  // lanes per row, rows per pass
   const long ldc = EPI == 2 ? N / 2 : N;
   const long ccol = EPI == 2 ? cbase / 2 : cbase;
+  C += (long)ks * M * ldc;  // this split's partial
   constexpr int NPASS = 32 / RPP;
   // residual operand of one pass: V values of row `row` from column `oc`
   using RRaw = typename std::conditional<std::is_same<TR, float>::value, float4,
@@ -676,7 +685,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 // ==================================================================== launch
 template <int EPI, typename TR, typename TC>
-static int launch_tile(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st) {
+static int launch_tile(int M, int N, int K, const void* A, const void* W, const void* R, void* C, hipStream_t st,
+                       int splits = 1) {
   static_assert(tile::LDS_BYTES <= 160 * 1024, "LDS per workgroup");
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_tile_kernel<EPI, TR, TC>,
                                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)tile::LDS_BYTES);
@@ -684,14 +694,115 @@ static int launch_tile(int M, int N, int K, const void* A, const void* W, const 
   const int tiles_m = (M + tile::BM - 1) / tile::BM, tiles_n = N / tile::BN;
   // wide outputs walk 8 tile-rows per group (more W reuse per XCD), narrow 4
   const int group = tiles_n >= 64 ? 8 : 4;
-  hipLaunchKernelGGL((gemm_tile_kernel<EPI, TR, TC>), dim3(tiles_m * tiles_n), dim3(tile::NT), tile::LDS_BYTES, st,
-                     (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n, group);
+  hipLaunchKernelGGL((gemm_tile_kernel<EPI, TR, TC>), dim3(tiles_m * tiles_n * splits), dim3(tile::NT),
+                     tile::LDS_BYTES, st, (const bf16_t*)A, (const bf16_t*)W, (const TR*)R, (TC*)C, M, N, K, tiles_n,
+                     group, splits);
   return 0;
+}
+
+static int compute_units() {
+  static const int n = [] {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                 hipSuccess || v <= 0)
+      return 256;
+    return v;
+  }();
+  return n;
+}
+
+// Rounds of a launch of `wgs` tile workgroups (one resident per compute
+// unit: the tile kernel takes the whole register file) times the stages per
+// workgroup, plus the split partials' traffic (written, then read once by
+// the consumer) in stage-times: one 256x256x64 stage is ~1.2 us at the
+// power-capped MFMA clock, in which HBM moves ~6 MB.
+static double tile_cost(long tiles, int T, int S, long M, long N) {
+  const long cu = compute_units();
+  const long rounds = (tiles * S + cu - 1) / cu;
+  return (double)rounds * ((T + S - 1) / S) + (S > 1 ? (double)S * M * N * 8.0 / 6.0e6 : 0.0);
+}
+
+int gemm_tile_splits(int M, int N, int K) {
+  using namespace tile;
+  if (M <= skinny::MAXM || N % BN || K % BK) return 1;
+  const long tiles = (long)((M + BM - 1) / BM) * (N / BN);
+  const int T = K / BK;
+  int best = 1;
+  double best_cost = tile_cost(tiles, T, 1, M, N);
+  for (int S = 2; S <= 4 && T / S >= 16; ++S) {
+    const double c = tile_cost(tiles, T, S, M, N);
+    if (c < best_cost) best = S, best_cost = c;
+  }
+  return best;
+}
+
+size_t gemm_tile_partials_bound(int max_rows, int N, int K) {
+  size_t b = 0;
+  for (int m = tile::BM;; m += tile::BM) {
+    const int mm = std::min(m, max_rows);
+    const int S = gemm_tile_splits(mm, N, K);
+    if (S > 1) b = std::max(b, (size_t)S * mm * N * sizeof(float));
+    if (mm == max_rows) break;
+  }
+  return b;
+}
+
+int launch_gemm_tile_split(int M, int N, int K, int S, const void* A, const void* W, float* part, hipStream_t st) {
+  if (M <= 0 || S < 1 || N % tile::BN || K % tile::BK || K / tile::BK < S) return -1;
+  return launch_tile<0, float, float>(M, N, K, A, W, nullptr, part, st, S);
+}
+
+template <int EPI, typename TR, typename TC>
+static int launch_reduce(int M, int N, int S, const float* part, const void* R, void* C, hipStream_t st);
+
+int launch_split_residual(int r_dt, int c_dt, int M, int N, int S, const float* part, const void* R, void* C,
+                          hipStream_t st) {
+  if (M == 0) return 0;
+  if (r_dt == 0 && c_dt == 1) return launch_reduce<1, float, bf16_t>(M, N, S, part, R, C, st);
+  if (r_dt == 1 && c_dt == 1) return launch_reduce<1, bf16_t, bf16_t>(M, N, S, part, R, C, st);
+  if (r_dt == 1 && c_dt == 0) return launch_reduce<1, bf16_t, float>(M, N, S, part, R, C, st);
+  if (r_dt == 0 && c_dt == 0) return launch_reduce<1, float, float>(M, N, S, part, R, C, st);
+  return -1;
+}
+
+template <typename TR, typename TC>
+__global__ __launch_bounds__(256) void gemm_reduce_residual4_kernel(const float* __restrict__ part,
+                                                                    const TR* __restrict__ R, TC* __restrict__ C,
+                                                                    long n4, long mn, int S) {
+  for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < n4; e += (long)gridDim.x * 256) {
+    float4 v = ((const float4*)part)[e];
+    for (int s = 1; s < S; ++s) {
+      const float4 p = ((const float4*)(part + s * mn))[e];
+      v.x += p.x, v.y += p.y, v.z += p.z, v.w += p.w;
+    }
+    if constexpr (std::is_same<TR, float>::value) {
+      const float4 r = ((const float4*)R)[e];
+      v.x += r.x, v.y += r.y, v.z += r.z, v.w += r.w;
+    } else {
+      const uint2 r = ((const uint2*)R)[e];
+      v.x += __uint_as_float(r.x << 16), v.y += __uint_as_float(r.x & 0xffff0000u);
+      v.z += __uint_as_float(r.y << 16), v.w += __uint_as_float(r.y & 0xffff0000u);
+    }
+    if constexpr (std::is_same<TC, float>::value)
+      ((float4*)C)[e] = v;
+    else
+      ((uint2*)C)[e] = uint2{pack_bf2(v.x, v.y), pack_bf2(v.z, v.w)};
+  }
 }
 
 template <int EPI, typename TR, typename TC>
 static int launch_reduce(int M, int N, int S, const float* part, const void* R, void* C, hipStream_t st) {
   const long total = (EPI == 2) ? (long)M * (N / 2) : (long)M * N;
+  if constexpr (EPI == 1) {
+    auto al = [](const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; };
+    if (N % 4 == 0 && al(part, 16) && al(R, 4 * sizeof(TR)) && al(C, 4 * sizeof(TC))) {
+      const long n4 = total / 4;
+      const int blocks = (int)std::min<long>((n4 + 255) / 256, 8192);
+      hipLaunchKernelGGL((gemm_reduce_residual4_kernel<TR, TC>), dim3(blocks), dim3(256), 0, st, part, (const TR*)R,
+                         (TC*)C, n4, total, S);
+      return 0;
+    }
+  }
   int blocks = (int)std::min<long>((total + 255) / 256, 4096);
   hipLaunchKernelGGL((gemm_reduce_kernel<EPI, TR, TC>), dim3(blocks), dim3(256), 0, st, part, (const TR*)R, (TC*)C,
                      M, N, S);

@@ -55,6 +55,19 @@ struct SkinnyPlan {
 };
 SkinnyPlan gemm_skinny_plan(int M, int N, int K);
 int gemm_check(int dtype, int epi, int M, int N, int K);
+// K splits (1..4) for a tile-path GEMM (M > 64) whose fp32 partials a fused
+// consumer sums: chosen to cut the launch's rounds over the compute units,
+// weighed against the partials' traffic. 1 for the skinny path.
+int gemm_tile_splits(int M, int N, int K);
+// Largest partial bytes gemm_tile_splits leads to for any M <= max_rows.
+size_t gemm_tile_partials_bound(int max_rows, int N, int K);
+// The tile GEMM's K-split partials: fp32 part[S][M][N] (A W^T over split s's
+// near-equal stage range), summed in split order by the consumer.
+int launch_gemm_tile_split(int M, int N, int K, int S, const void* A, const void* W, float* part, hipStream_t st);
+// part[S][M][N] summed in split order plus the residual R (fp32 or bf16),
+// into C (the residual epilogue of a split GEMM).
+int launch_split_residual(int r_dt, int c_dt, int M, int N, int S, const float* part, const void* R, void* C,
+                          hipStream_t st);
 // Split-K partial bytes a launch really uses (0 when nothing is split).
 size_t gemm_partials_bytes(int dtype, int epi, int M, int N, int K);
 // Size of the static split-K scratch array (PS_GEMM_STATIC_SCRATCH_BYTES).

@@ -79,6 +79,32 @@ def test_prefill_8x2048_sampled_sequences(layer8b):
         normwise_ok(got[(b + 1) * T - 1], ref, f"seq {b} row {T - 1}")
 
 
+def test_prefill_5x416_three_way_k_split(layer8b):
+    """2080 prefill rows: nine 256-row tile rows, so the down GEMM's 144
+    tiles are split three ways in K (432 workgroups, two rounds instead of
+    one at full K) and summed with the residual by the reduce kernel. The
+    last prompt is compared in full, every other prompt on its last row."""
+    wl, sh = layer8b["wl"], layer8b["wl"].shape
+    n, T = 5, 416
+    pool = H.Pool(sh, n * T // 16 + 8, n, T // 16, seed=gen.page_order_seed(wl))
+    layer = B.Layer(pool.cfg)
+    seqs = [pool.kv.open() for _ in range(n)]
+    for s in seqs:
+        pool.kv.alloc(s, T)
+    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, n * T, n, T // 16))
+    x = gen.prefill_input(wl, n * T)
+    out = H.empty((n * T, sh.hidden), "bf16")
+    layer.prefill(layer8b["dev"].w, pool.kv, 0, seqs, [T] * n, H.to_dev(x, "bf16"), out, ws)
+    sync()
+    got = H.to_f64(out)
+    xf = gen.widen(x, "bf16")
+    ref = O.layer_sequence(layer8b["wf"], sh, xf[(n - 1) * T:])["out"]
+    normwise_ok(got[(n - 1) * T:], ref, f"prefill seq {n - 1}")
+    for b in range(n - 1):
+        r = O.layer_rows(layer8b["wf"], sh, xf[b * T:(b + 1) * T], [T - 1])[0]
+        normwise_ok(got[(b + 1) * T - 1], r, f"seq {b} row {T - 1}")
+
+
 def _decode_fullsize(layer8b, wl, sample, phase, mixed=False):
     sh = wl.shape
     ctx = [int(c) for c in gen.context_lengths(wl)]
@@ -127,7 +153,9 @@ def _decode_fullsize(layer8b, wl, sample, phase, mixed=False):
         ref = O.layer_sequence(layer8b["wf"], sh, xf[off + b:off + b + 1], *hist[b])["out"][0]
         normwise_ok(got[off + b], ref, f"decode seq {b} ctx {ctx[b]}", tol)
     if mixed:
-        for i in (0, nc - 1):
+        # every chunk: together they span every tile row of the chunk rows'
+        # K-split O and down launches
+        for i in range(nc):
             ref = O.layer_sequence(layer8b["wf"], sh, xf[i * chunk:(i + 1) * chunk])["out"]
             normwise_ok(got[i * chunk:(i + 1) * chunk], ref, f"mixed chunk {i}")
     return ctx
