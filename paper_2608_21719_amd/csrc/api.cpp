@@ -1035,8 +1035,11 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
     if (fused_norm) {
       S = gemm_tile_splits(n, d, dq);
       if (S > 1) {
-        if (ws_bytes < (size_t)S * n * d * 4) bad |= 1;
-        else bad |= launch_gemm_tile_split(n, d, dq, S, a, w->w_o, (float*)ws, s);
+        if (ws_bytes < (size_t)S * n * d * 4) {  // the layout's bound rules this out
+          bad |= 1;
+          return;
+        }
+        bad |= launch_gemm_tile_split(n, d, dq, S, a, w->w_o, (float*)ws, s);
       } else {
         bad |= launch_gemm_split(dt, dt, PS_F32, PS_EPI_RESIDUAL, n, d, dq, a, w->w_o, res, hr, ws, ws_bytes, s, &S);
       }
@@ -1056,7 +1059,7 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
     char* y = (char*)x_out + (size_t)r0 * d * eb;
     const int S = dt == PS_BF16 ? gemm_tile_splits(n, d, c.ffn) : 1;
     if (S > 1) {
-      if (ws_bytes < (size_t)S * n * d * 4) {
+      if (ws_bytes < (size_t)S * n * d * 4) {  // the layout's bound rules this out
         bad |= 1;
         return;
       }
