@@ -711,11 +711,12 @@ static int compute_units() {
   return n;
 }
 
-// Rounds of a launch of `wgs` tile workgroups (one resident per compute
-// unit: the tile kernel takes the whole register file) times the stages per
-// workgroup, plus the split partials' traffic (written, then read once by
-// the consumer) in stage-times: one 256x256x64 stage is ~1.2 us at the
-// power-capped MFMA clock, in which HBM moves ~6 MB.
+// Cost of a tile-kernel launch of `tiles` tiles split S ways in K: rounds of
+// workgroups over the compute units (one resident per unit: the kernel takes
+// the whole register file) times the stages per workgroup, plus the split
+// partials' traffic (written, then read once by the consumer) in stage-times:
+// one 256x256x64 stage is ~1.2 us at the power-capped MFMA clock, in which
+// HBM moves ~6 MB.
 static double tile_cost(long tiles, int T, int S, long M, long N) {
   const long cu = compute_units();
   const long rounds = (tiles * S + cu - 1) / cu;
