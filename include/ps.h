@@ -376,8 +376,8 @@ ps_status ps_decode_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t la
  * rows' attention and O/down GEMMs go to a second stream that the layer
  * handle creates on first use (default priority, on the caller's device),
  * joined back into `stream` by events before the call returns: the caller
- * sees one stream's ordering. A layer handle (and a model handle, whose
- * mixed calls do the same) is used by one host thread at a time. */
+ * sees one stream's ordering. A layer handle is used by one host thread at a
+ * time. */
 ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_chunk,
                         const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec,
                         const int32_t* dec_seqs, const void* x_in, void* x_out, void* ws,

@@ -224,8 +224,9 @@ struct ps_kv {
 };
 
 // A second stream on the caller's device (default priority, non-blocking)
-// and the events that fork work onto it and join it back inside one call.
-// Created on first use; a handle is driven by one host thread at a time.
+// and the events that fork a mixed step's work onto it and join it back
+// inside one call. Created on first use; a layer handle is driven by one host
+// thread at a time.
 struct AuxStream {
   static constexpr int kEvents = 4;
   int dev = -1;
@@ -279,7 +280,6 @@ struct ps_layer {
 
 struct ps_model {
   ps_layer_cfg cfg;
-  AuxStream aux;
   int32_t n_layers = 0, vocab = 0;
   const void* embed = nullptr;
   const void* final_norm = nullptr;
@@ -1232,16 +1232,13 @@ ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, cons
   const ModelWs mw = model_layout(c, M->vocab, P.wl.total, P.rows, n_out);
   if (ps_status rc = check_ws(ws, ws_bytes, mw.total)) return rc;
   hipStream_t st = (hipStream_t)stream;
-  AuxStream* aux = nullptr;
-  if (n_chunk > 0 && n_dec > 0)
-    if (ps_status rc = M->aux.get(st, &aux)) return rc;
   if (ps_status rc = upload_meta(kv, P.mt, ws, st)) return rc;
   char* W = (char*)ws;
   int bad = launch_embed(P.rows, c.hidden, M->vocab, M->embed, tokens, W + mw.xa, st);
   char* cur = W + mw.xa;
   char* nxt = W + mw.xb;
   for (int l = 0; l < M->n_layers; ++l) {
-    bad |= launch_layer(c, P, &M->layers[l], kv->layer_base(l), cur, nxt, W, st, nullptr, aux);
+    bad |= launch_layer(c, P, &M->layers[l], kv->layer_base(l), cur, nxt, W, st);
     std::swap(cur, nxt);
   }
   float* logits = logits_out ? logits_out : (float*)(W + mw.logits);
