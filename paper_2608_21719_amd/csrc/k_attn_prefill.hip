@@ -4,8 +4,8 @@
 // A workgroup owns one 32-row query tile (32 * kFaQB rows, kFaQB = 1) of one
 // sequence and one KV head; its waves are four query heads of that group
 // (two workgroups per KV head when G = 8), so every K/V tile staged
-// in LDS serves all of them (GQA reuse). Keys are walked in 64-key tiles
-// (four pages) from position 0 up to the tile's last query position; the
+// in LDS serves all of them (GQA reuse). Keys are walked in 32-key tiles
+// (two pages) from position 0 up to the tile's last query position; the
 // cached prefix of a chunked prefill is just the first pages of the walk.
 //
 // Both products are arranged so that softmax statistics never cross lanes:
@@ -17,16 +17,21 @@
 // and O^T, so the online-softmax rescale is lane-local and the S^T
 // accumulator, exponentiated and rounded to bf16, is already the B operand
 // of the PV product. The V^T pages (dimension-major) make the A operand a
-// contiguous read. LDS rows are padded (272 B for K, 144 B for V^T) so the
+// contiguous read. LDS rows are padded (272 B for K, 80 B for V^T) so the
 // 16-byte operand reads of 16 consecutive lanes hit disjoint banks.
 //
-// The pass is bound by the vector ALU (the softmax), not the matrix cores,
-// so the per-score vector work is kept minimal: the running max is taken on
+// The matrix cores are busy about a third of the time: each MFMA waits on
+// its own LDS operand read and the softmax sits between the two products.
+// The per-score vector work is kept minimal: the running max is taken on
 // raw scores and the scale folds into one FMA per exponent, the output is
 // rescaled only when a row's max outgrows the exponent base by 2^8, and the row sum
-// l comes from the matrix cores as a fifth O^T block whose A operand is all
-// ones (so l is the fp32 sum of exactly the bf16 P values the PV product
-// uses, and V == 1 gives exactly 1).
+// l is one packed bf16 dot product (v_dot2, against ones) per pair of P values,
+// accumulated in fp32: the sum of exactly the bf16 P values the PV product
+// uses, so V == 1 gives 1 to fp32 rounding, exactly 1 after the bf16 store.
+//
+// The short tiles keep the LDS footprint at 45 KB and the registers at 168
+// per lane, so three workgroups (three waves per SIMD) share a CU; their
+// interleaving hides the LDS and global latency one wave cannot.
 #include "common.h"
 #include "launch.h"
 
@@ -34,7 +39,7 @@ namespace ps {
 
 namespace {
 constexpr int kHd = 128;
-constexpr int kFaKT = 64;            // keys per tile (four pages)
+constexpr int kFaKT = 32;            // keys per tile (two pages)
 constexpr int kPageCache = 2048;     // page ids cached in LDS (32768 positions)
 constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: lower register pressure, 2.3x faster than 2)
 }  // namespace
@@ -45,7 +50,7 @@ constexpr int kFaQB = 1;             // query blocks of 32 rows per wave (1: low
 // tile's products, and written to the other LDS buffer after them, so one
 // barrier per tile suffices and load latency hides behind the MFMAs.
 template <int QB, int KT>  // 32-row query blocks per wave (query tile 32 * QB rows); keys per tile
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
                                                          const int32_t* __restrict__ bt,
@@ -116,20 +121,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
     for (int kk = 0; kk < 8; ++kk) qf[cb][kk] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * kk));
   }
 
-  // oacc[cb][0..3]: O^T dims 32 db + ...; oacc[cb][4]: every row is l (ones block)
-  f32x16_t oacc[QB][5];
+  // oacc[cb][db]: O^T dims 32 db + ...; lsum: this lane's half of l (keys with offset 4g)
+  f32x16_t oacc[QB][4];
+  float lsum[QB];
+#pragma unroll
+  for (int cb = 0; cb < QB; ++cb) lsum[cb] = 0.f;
 #pragma unroll
   for (int cb = 0; cb < QB; ++cb)
 #pragma unroll
-    for (int db = 0; db < 5; ++db)
+    for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[cb][db][r] = 0.f;
   float m[QB];  // exponent base of each row block (raw, unscaled score units)
 #pragma unroll
   for (int cb = 0; cb < QB; ++cb) m[cb] = -INFINITY;
-  bf16x8_t ones;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   // staging assignment: load i of thread t covers page i of the tile: K row
   // t / 16, 16-byte chunk t % 16; V^T dim t / 2, keys 8 (t % 2) .. + 8. The
@@ -250,9 +257,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
         const float m_new = fmaxf(m[cb], mx);
         const float alpha = __builtin_amdgcn_exp2f((m[cb] - m_new) * scale_log2);  // lane-local factor
 #pragma unroll
-        for (int db = 0; db < 5; ++db)
+        for (int db = 0; db < 4; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[cb][db][r] *= alpha;
+        lsum[cb] *= alpha;
         m[cb] = m_new;
       }
       const float mb = m[cb] * scale_log2;
@@ -262,6 +270,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
         for (int i = 0; i < 8; ++i)
           pk[kb][cb][i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[kb][cb][2 * i], scale_log2, -mb)),
                                    __builtin_amdgcn_exp2f(fmaf(sacc[kb][cb][2 * i + 1], scale_log2, -mb)));
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          lsum[cb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[kb][cb][i]), ones2, lsum[cb], false);
     }
     // O^T += V^T P^T per page (16 keys) and row block, each V fragment read once
 #pragma unroll
@@ -280,9 +293,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
         for (int cb = 0; cb < QB; ++cb)
           if (act[cb]) oacc[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp[cb], oacc[cb][db], 0, 0, 0);
       }
-#pragma unroll
-      for (int cb = 0; cb < QB; ++cb)
-        if (act[cb]) oacc[cb][4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, bp[cb], oacc[cb][4], 0, 0, 0);
     }
     if (kt + 1 < n_tiles) lstore(buf ^ 1);
     __syncthreads();
@@ -291,9 +301,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
   // ---- normalise and store: lane holds query c, dims 32db + 8(r/4) + 4g + r%4
 #pragma unroll
   for (int cb = 0; cb < QB; ++cb) {
+    const float l = lsum[cb] + __shfl_xor(lsum[cb], 32);
     const int r0 = 32 * cb + c;
     if (r0 >= qn) continue;
-    const float inv = 1.f / oacc[cb][4][0];  // l of query c (every row of the ones block)
+    const float inv = 1.f / l;
     bf16_t* op = o + ((long)(s.row_start + it.q_begin + r0) * n_q + head) * kHd;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
