@@ -126,14 +126,16 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
     # flash attention alone over the K/V the last step wrote (lengths are 0 again)
     qa = randn(torch, gen, (tokens, sh.n_q, sh.head_dim))
     oa = torch.empty((tokens, sh.d_q), dtype=torch.bfloat16, device="cuda")
-    a_ms = timer(lambda: B.op_attention(kv, 0, seqs, [T] * n, qa, oa, ws), iters=max(5, steps))
+    attn_run = lambda: B.op_attention(kv, 0, seqs, [T] * n, qa, oa, ws)  # noqa: E731
+    a_ms = timer(attn_run, iters=max(5, steps))
+    tel_attn = observe(attn_run)
     traffic = measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
     res = {
         "tok_s": tokens / (ms * 1e-3), "ms_per_step": ms,
         "layer_tflops": (total_gemm + attn) / (ms * 1e-3) / 1e12,
         "telemetry": tel_step,
         "gate_up_gemm": {"ms": g_ms, "tflops": gemm_tflops, "M": M, "N": N, "K": K, "telemetry": tel_gemm},
-        "attention": {"ms": a_ms, "tflops": attn / (a_ms * 1e-3) / 1e12},
+        "attention": {"ms": a_ms, "tflops": attn / (a_ms * 1e-3) / 1e12, "telemetry": tel_attn},
         "roofline": A.Roofline("mfma", gemm_tflops, A.BF16_DENSE_PEAK_TFLOPS, "TFLOP/s", traffic,
                                roofline_extra("mfma", gemm_tflops, tel_gemm, traffic)).as_dict(),
     }

@@ -1,6 +1,6 @@
 """Build libps.so (gfx950 HIP kernels + C ABI) in-tree with hipcc.
 
-Usage: python -m paper_2608_21719_amd.build [--jobs N]
+Usage: python -m paper_2608_21719_amd.build [--jobs N] [--probes]
 
 Every source is compiled to its own object in parallel, then linked into
 ``paper_2608_21719_amd/libps.so`` next to this file. All device code is built
@@ -60,6 +60,27 @@ def build(jobs: int = 8, verbose: bool = True) -> str:
     return LIB
 
 
+def build_probes(verbose: bool = True) -> list:
+    """Standalone measurement programs under probes/ (not linked into libps):
+    each ``probes/<name>.hip`` becomes the executable ``probes/<name>``."""
+    pdir = os.path.join(HERE, "probes")
+    built = []
+    for f in sorted(os.listdir(pdir)) if os.path.isdir(pdir) else []:
+        if not f.endswith(".hip"):
+            continue
+        src, exe = os.path.join(pdir, f), os.path.join(pdir, f[:-4])
+        cmd = [HIPCC, "-O3", "-std=c++17", f"--offload-arch={ARCH}",
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-Wno-unused-result", src, "-o", exe]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n" + r.stdout + r.stderr)
+        built.append(exe)
+    if verbose and built:
+        print("built probes: " + ", ".join(os.path.basename(x) for x in built))
+    return built
+
+
 def clean():
     shutil.rmtree(os.path.join(HERE, "_build"), ignore_errors=True)
 
@@ -67,5 +88,8 @@ def clean():
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
+    ap.add_argument("--probes", action="store_true", help="also build the measurement programs in probes/")
     a = ap.parse_args()
     build(a.jobs)
+    if a.probes:
+        build_probes()

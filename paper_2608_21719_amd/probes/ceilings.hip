@@ -1,0 +1,146 @@
+// Attainable ceilings of one MI355X (gfx950), measured rather than taken
+// from the data sheet: HBM streaming read and copy bandwidth, the dense
+// bf16 MFMA rate of v_mfma_f32_32x32x16_bf16 on register operands, and
+// whether MFMA and vector-ALU work issued on the same SIMD overlap in time.
+// A standalone program (not part of libps); every buffer is allocated here
+// and every kernel indexes inside it.
+#include <hip/hip_runtime.h>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#define CHECK(x)                                                                 \
+  do {                                                                           \
+    hipError_t e_ = (x);                                                         \
+    if (e_ != hipSuccess) {                                                      \
+      std::fprintf(stderr, "%s failed: %s\n", #x, hipGetErrorString(e_));       \
+      std::exit(1);                                                              \
+    }                                                                            \
+  } while (0)
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// grid-stride non-temporal 16-byte reads, folded so the loads stay live
+__global__ void hbm_read(const u32x4* __restrict__ p, long n, unsigned* out) {
+  u32x4 acc = {0, 0, 0, 0};
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    acc ^= __builtin_nontemporal_load(p + i);
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) out[0] = 1;
+}
+
+__global__ void hbm_copy(const u32x4* __restrict__ p, u32x4* __restrict__ q, long n) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) q[i] = p[i];
+}
+
+// MODE 0: MFMA only; 1: vector FMAs only; 2: both in every wave (accumulators
+// in VGPRs); 3: both, accumulators held in AGPRs. Four independent 32x32
+// accumulators and four independent FMA chains per wave.
+template <int MODE>
+__global__ __launch_bounds__(256) void issue_mix(float* out, int iters) {
+  f32x16 acc[4];
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  bf16x8 a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(1e-3f * (float)(threadIdx.x + e));
+    b[e] = (__bf16)(2e-3f * (float)e);
+  }
+  float v0 = threadIdx.x * 1e-3f, v1 = v0 + 1.f, v2 = v0 + 2.f, v3 = v0 + 3.f;
+  for (int i = 0; i < iters; ++i) {
+    if (MODE != 1) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+        if (MODE == 3) asm volatile("" : "+a"(acc[j]));
+      }
+    }
+    if (MODE != 0) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        v0 = fmaf(v0, 1.0001f, 0.5f);
+        v1 = fmaf(v1, 0.9999f, 0.25f);
+        v2 = fmaf(v2, 1.0002f, 0.125f);
+        v3 = fmaf(v3, 0.9998f, 0.0625f);
+      }
+    }
+  }
+  float s = v0 + v1 + v2 + v3;
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) s += acc[j][r];
+  out[(long)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+static float time_ms(hipEvent_t e0, hipEvent_t e1) {
+  float ms = 0.f;
+  CHECK(hipEventElapsedTime(&ms, e0, e1));
+  return ms;
+}
+
+int main() {
+  int dev = 0, cus = 0;
+  CHECK(hipGetDevice(&dev));
+  CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  hipEvent_t e0, e1;
+  CHECK(hipEventCreate(&e0));
+  CHECK(hipEventCreate(&e1));
+
+  // ---- HBM: 4 GiB source, far beyond the caches
+  const long bytes = 4L << 30, n = bytes / 16;
+  u32x4 *a = nullptr, *b = nullptr;
+  unsigned* flag = nullptr;
+  CHECK(hipMalloc(&a, bytes));
+  CHECK(hipMalloc(&b, bytes / 2));
+  CHECK(hipMalloc(&flag, 4));
+  CHECK(hipMemset(a, 1, bytes));
+  CHECK(hipDeviceSynchronize());
+  double best_rd = 0, best_cp = 0;
+  for (int grid : {1024, 2048, 4096, 8192}) {
+    hipLaunchKernelGGL(hbm_read, dim3(grid), dim3(256), 0, 0, a, n, flag);
+    CHECK(hipEventRecord(e0));
+    for (int i = 0; i < 10; ++i) hipLaunchKernelGGL(hbm_read, dim3(grid), dim3(256), 0, 0, a, n, flag);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    const double rd = 10.0 * bytes / (time_ms(e0, e1) * 1e-3) / 1e9;
+    // copy half the source into b: bytes / 2 read + bytes / 2 written
+    hipLaunchKernelGGL(hbm_copy, dim3(grid), dim3(256), 0, 0, a, b, n / 2);
+    CHECK(hipEventRecord(e0));
+    for (int i = 0; i < 10; ++i) hipLaunchKernelGGL(hbm_copy, dim3(grid), dim3(256), 0, 0, a, b, n / 2);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    const double cp = 10.0 * bytes / (time_ms(e0, e1) * 1e-3) / 1e9;
+    std::printf("hbm  grid %5d x 256: read %6.0f GB/s   copy %6.0f GB/s (read + write)\n", grid, rd, cp);
+    best_rd = rd > best_rd ? rd : best_rd;
+    best_cp = cp > best_cp ? cp : best_cp;
+  }
+  CHECK(hipGetLastError());
+  CHECK(hipFree(a));
+  CHECK(hipFree(b));
+  CHECK(hipFree(flag));
+
+  // ---- matrix cores and vector ALU: two workgroups of four waves per CU
+  // (two waves per SIMD); the first timed pass follows a long warm-up so the
+  // clock has settled
+  const int blocks = 2 * cus, iters = 20000;
+  float* out = nullptr;
+  CHECK(hipMalloc(&out, (size_t)blocks * 256 * sizeof(float)));
+  auto run = [&](auto kern) {
+    for (int w = 0; w < 3; ++w) hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, 0, out, iters);
+    CHECK(hipEventRecord(e0));
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, 0, out, iters);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    return (double)time_ms(e0, e1);
+  };
+  const double t_m = run(issue_mix<0>), t_v = run(issue_mix<1>), t_b = run(issue_mix<2>), t_a = run(issue_mix<3>);
+  CHECK(hipGetLastError());
+  const double mfma_flop = (double)blocks * 4 * iters * 4 * (32.0 * 32 * 16 * 2);
+  std::printf("mfma 32x32x16 bf16, register operands: %.0f TFLOP/s (%.3f ms)\n", mfma_flop / (t_m * 1e-3) / 1e12, t_m);
+  std::printf("vector fp32 FMA only:                   %.3f ms\n", t_v);
+  std::printf("both in every wave, VGPR accumulators:  %.3f ms  (sum of the two alone %.3f ms)\n", t_b, t_m + t_v);
+  std::printf("both in every wave, AGPR accumulators:  %.3f ms\n", t_a);
+  std::printf("best: hbm read %.0f GB/s, hbm copy %.0f GB/s\n", best_rd, best_cp);
+  CHECK(hipFree(out));
+  return 0;
+}
