@@ -365,19 +365,19 @@ ps_status ps_decode_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t la
 
 /* Mixed step (chunked prefill fused with decode; §II-B's phases served by one
  * batch, as the serving systems the paper builds on do when new requests
- * join a running decode batch): the GEMMs run once over
- * the concatenated rows — first the chunk rows of n_chunk sequences
- * (chunk_tok[i] rows each), then one row for each of n_dec decoding
- * sequences; attention uses the prefill path for chunk rows and the split-K
- * decode path for decode rows. Same result as separate ps_prefill and
- * ps_decode_step calls up to rounding.
+ * join a running decode batch). The rows are concatenated: first the chunk
+ * rows of n_chunk sequences (chunk_tok[i] rows each), then one row for each
+ * of n_dec decoding sequences. The norm, QKV GEMM and RoPE + KV write run
+ * once over all rows; attention uses the prefill path for chunk rows and
+ * the split-K decode path for decode rows. Same result as separate
+ * ps_prefill and ps_decode_step calls up to rounding.
  * With more than 64 chunk rows and at most 64 decode rows (bf16, d a
  * multiple of 8 up to 8192) the call forks after the KV write: the decode
- * rows' attention and O/down GEMMs go to a second stream that the layer
- * handle creates on first use (default priority, on the caller's device),
- * joined back into `stream` by events before the call returns: the caller
- * sees one stream's ordering. A layer handle is used by one host thread at a
- * time. */
+ * rows' attention and the rest of their layer (O, SwiGLU and down GEMMs)
+ * go to a second stream that the layer handle creates on first use
+ * (default priority, on the caller's device), joined back into `stream` by
+ * an event before the call returns: the caller sees one stream's ordering.
+ * A layer handle is used by one host thread at a time. */
 ps_status ps_mixed_step(ps_layer* L, const ps_layer_w* w, ps_kv* kv, int32_t layer, int32_t n_chunk,
                         const int32_t* chunk_seqs, const int32_t* chunk_tok, int32_t n_dec,
                         const int32_t* dec_seqs, const void* x_in, void* x_out, void* ws,

@@ -228,7 +228,7 @@ struct ps_kv {
 // inside one call. Created on first use; a layer handle is driven by one host
 // thread at a time.
 struct AuxStream {
-  static constexpr int kEvents = 4;
+  static constexpr int kEvents = 2;
   int dev = -1;
   hipStream_t s = nullptr;
   hipEvent_t ev[kEvents] = {};
@@ -605,11 +605,12 @@ WsLayout layout(const ps_layer_cfg& c, size_t meta_bytes, int32_t rows, int32_t 
     g = std::max(g, gemm_tile_partials_bound(rows, (int)d, c.ffn));
   }
   L.gemm = take(g);
-  // the decode rows' O and down partials when they run on the second
-  // stream beside the chunk rows
+  // the decode rows' O, SwiGLU and down partials when they run on the
+  // second stream beside the chunk rows
   size_t gb = 0;
   if (gm > 0) {
     gb = std::max(gb, gemm_workspace_bytes(c.dtype, gm, (int)d, (int)dq));
+    gb = std::max(gb, gemm_workspace_bytes(c.dtype, gm, 2 * c.ffn, (int)d));
     gb = std::max(gb, gemm_workspace_bytes(c.dtype, gm, (int)d, c.ffn));
   }
   L.gemm_b = take(gb);
@@ -1077,13 +1078,14 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
       bad |= launch_attn_generic(dt, 0, P.chunk_rows, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr, pool, si,
                                  bt, o, scale, s);
   };
-  auto decode_attn = [&](hipStream_t s) {
+  auto decode_attn = [&](hipStream_t s, int max_wg) {
     if (P.dec_mfma) {
       const char* qd = qr + (size_t)P.chunk_rows * dq * eb;
       char* od = o + (size_t)P.chunk_rows * dq * eb;
       bad |= launch_decode_attn(G, P.n_ditems, c.n_kv_heads, P.n_dec, qd, pool, si + P.n_chunk, bt,
                                 (const DecodeItem*)(W + P.o_di), (float*)(W + wl.apart_o), (float*)(W + wl.apart_ml),
-                                (const int32_t*)(W + P.o_pb), (const int32_t*)(W + P.o_pc), od, scale_log2, s);
+                                (const int32_t*)(W + P.o_pb), (const int32_t*)(W + P.o_pc), od, scale_log2, s,
+                                max_wg);
     } else {
       bad |= launch_attn_generic(dt, P.chunk_rows, P.n_dec, P.n_seqs, c.n_q_heads, c.n_kv_heads, c.head_dim, qr,
                                  pool, si, bt, o, scale, s);
@@ -1103,15 +1105,15 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
                              c.n_kv_heads, c.head_dim, st, (const float*)gws, s_qkv);
 
   // A mixed batch (prefill chunks + decode rows) splits after the KV write:
-  // the decode rows' attention (HBM-bound over long contexts) and their
-  // skinny O and down GEMMs run on the second stream while the chunk rows'
-  // flash attention and tile GEMMs run on the caller's; the SwiGLU GEMM
-  // takes all rows at once. The two row sets write disjoint rows of o, h,
-  // xn and x_out, and each stream has its own split-K partials.
+  // the decode rows' attention (HBM-bound over long contexts) and the rest
+  // of their layer (skinny O, SwiGLU and down GEMMs, weight-bandwidth
+  // bound) run on the second stream while the chunk rows' flash attention
+  // and tile GEMMs run on the caller's. The two row sets write disjoint rows
+  // of o, h, xn, m and x_out, and each stream has its own split-K partials.
   const bool fork = aux && P.n_chunk > 0 && P.n_dec > 0 && P.n_dec <= 64 && P.chunk_rows > 64 && fused_norm;
   if (!fork) {
     if (P.n_chunk > 0) prefill_attn(st);
-    if (P.n_dec > 0) decode_attn(st);
+    if (P.n_dec > 0) decode_attn(st, 0);
     o_proj(0, rows, gws, gws_bytes, st);
     bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes,
                        st);
@@ -1124,17 +1126,23 @@ int launch_layer(const ps_layer_cfg& c, const LayerPlan& P, const ps_layer_w* w,
     if (hipEventRecord(aux->ev[i], from) != hipSuccess || hipStreamWaitEvent(to, aux->ev[i], 0) != hipSuccess)
       bad |= 1;
   };
+  auto swiglu = [&](int r0, int n, void* ws, size_t ws_bytes, hipStream_t s) {
+    bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, n, 2 * c.ffn, d, xn + (size_t)r0 * d * eb, w->w_gate_up, nullptr,
+                       m + (size_t)r0 * c.ffn * eb, ws, ws_bytes, s);
+  };
   link(st, sb, 0);
-  decode_attn(sb);
+  // the decode rows' attention on at most half as many workgroups as compute
+  // units, each walking several split items, so that it leaves compute units
+  // to the chunk rows' GEMMs (uncapped it takes them all while it runs)
+  decode_attn(sb, compute_units() / 2);
   o_proj(cr, P.n_dec, gws_b, gws_b_bytes, sb);
+  swiglu(cr, P.n_dec, gws_b, gws_b_bytes, sb);
+  down_proj(cr, P.n_dec, gws_b, gws_b_bytes, sb);
   prefill_attn(st);
   o_proj(0, cr, gws, gws_bytes, st);
-  link(sb, st, 1);
-  bad |= launch_gemm(dt, 0, dt, PS_EPI_SWIGLU, rows, 2 * c.ffn, d, xn, w->w_gate_up, nullptr, m, gws, gws_bytes, st);
-  link(st, sb, 2);
-  down_proj(cr, P.n_dec, gws_b, gws_b_bytes, sb);
+  swiglu(0, cr, gws, gws_bytes, st);
   down_proj(0, cr, gws, gws_bytes, st);
-  link(sb, st, 3);  // joined: the call's work is on the caller's stream again
+  link(sb, st, 1);  // joined: the call's work is on the caller's stream again
   return bad;
 }
 

@@ -9,7 +9,9 @@
 // on; the block table is read with scalar loads, so fetching the next page
 // id never waits on the vector loads already in flight. The kv head is the
 // fastest grid index: workgroups running together read the adjacent heads
-// of the same pages. Each page does all of the group's query heads at once
+// of the same pages. A launch may cap its workgroups (the mixed step does,
+// to leave compute units to the GEMMs beside it); each then walks items
+// y, y + gridDim.y, ... in turn. Each page does all of the group's query heads at once
 // on the matrix cores:
 //
 //   S^T[tok, head] = K[tok, :] . q[head, :]     4 x v_mfma_f32_16x16x32_bf16
@@ -39,11 +41,14 @@ template <int G>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_attn_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ pool, const SeqInfo* __restrict__ si,
     const int32_t* __restrict__ bt, const DecodeItem* __restrict__ items, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int n_kv, float scale_log2) {
+    float* __restrict__ part_ml, int n_kv, int n_items, float scale_log2) {
   static_assert(G <= 16, "one 16-row MFMA tile per KV group");
   constexpr int D = kPrefetch;
   const int kvh = blockIdx.x;
-  const DecodeItem it = items[blockIdx.y];
+  // items blockIdx.y, + gridDim.y, ...: one each when the grid covers them
+  // all, several when the launch caps its workgroups
+  for (int iy = blockIdx.y; iy < n_items; iy += gridDim.y) {
+  const DecodeItem it = items[iy];
   const SeqInfo s = si[it.b];
   const int kv_len = s.kv_before + s.n_new;
   const int n_q = n_kv * G;
@@ -221,6 +226,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
       part_ml[(part * G + head) * 2 + 1] = L;
     }
   }
+  __syncthreads();  // the next item reuses s_acc, s_m, s_l
+  }
 }
 
 // o[b, head, :] = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), splits in order.
@@ -247,16 +254,18 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(const float* __rest
 int launch_decode_attn(int G, int n_items, int n_kv, int n_seqs, const void* q, const void* pool_layer,
                        const SeqInfo* si, const int32_t* bt, const DecodeItem* items, float* part_o,
                        float* part_ml, const int32_t* part_begin, const int32_t* part_count, void* o,
-                       float scale_log2, hipStream_t st) {
+                       float scale_log2, hipStream_t st, int max_wg) {
   if (n_seqs == 0) return 0;
   if (n_items > kMaxDecodeItems) return -1;
-  dim3 grid(n_kv, n_items);
+  int gy = n_items;
+  if (max_wg > 0) gy = std::max(1, std::min(n_items, max_wg / n_kv));
+  dim3 grid(n_kv, gy);
   switch (G) {
-    case 1: hipLaunchKernelGGL(decode_attn_kernel<1>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
-    case 2: hipLaunchKernelGGL(decode_attn_kernel<2>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
-    case 4: hipLaunchKernelGGL(decode_attn_kernel<4>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
-    case 8: hipLaunchKernelGGL(decode_attn_kernel<8>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
-    case 16: hipLaunchKernelGGL(decode_attn_kernel<16>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, scale_log2); break;
+    case 1: hipLaunchKernelGGL(decode_attn_kernel<1>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, n_items, scale_log2); break;
+    case 2: hipLaunchKernelGGL(decode_attn_kernel<2>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, n_items, scale_log2); break;
+    case 4: hipLaunchKernelGGL(decode_attn_kernel<4>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, n_items, scale_log2); break;
+    case 8: hipLaunchKernelGGL(decode_attn_kernel<8>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, n_items, scale_log2); break;
+    case 16: hipLaunchKernelGGL(decode_attn_kernel<16>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt, items, part_o, part_ml, n_kv, n_items, scale_log2); break;
     default: return -1;
   }
   hipLaunchKernelGGL(decode_combine_kernel, dim3(n_seqs, n_kv * G), dim3(kHd), 0, st, part_o, part_ml,

@@ -700,7 +700,7 @@ static int launch_tile(int M, int N, int K, const void* A, const void* W, const 
   return 0;
 }
 
-static int compute_units() {
+int compute_units() {
   static const int n = [] {
     int dev = 0, v = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) !=

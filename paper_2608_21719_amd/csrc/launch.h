@@ -35,10 +35,11 @@ int launch_kv_gather(int dt, int len, const void* pool_layer, const int32_t* bt,
 int launch_decode_attn(int G, int n_items, int n_kv, int n_seqs, const void* q, const void* pool_layer,
                        const SeqInfo* si, const int32_t* bt, const DecodeItem* items, float* part_o,
                        float* part_ml, const int32_t* part_begin, const int32_t* part_count, void* o,
-                       float scale_log2, hipStream_t st);
+                       float scale_log2, hipStream_t st, int max_wg = 0);  // max_wg > 0: at most that many workgroups
 int launch_attn_generic(int dt, int row0, int rows, int n_seqs, int n_q, int n_kv, int hd, const void* q,
                         const void* pool_layer, const SeqInfo* si, const int32_t* bt, void* o, float scale,
                         hipStream_t st);
+int compute_units();  // of the current device (256 if the query fails)
 int fa_query_tile();  // query rows per prefill work item
 int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
                       const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st);
