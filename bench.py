@@ -27,6 +27,7 @@ if ROOT not in sys.path:
 
 METRIC = "decode tok/s & HBM GB/s; prefill tok/s & MFMA util (8B-shaped layer)"
 TEL = None  # telemetry.Telemetry, set in main: GPU clock and power of each timed leg
+TEL_SECONDS = 1.5  # length of each leg's clock-and-power window (0: none, e.g. under a counter profiler)
 
 
 def log(*a):
@@ -522,9 +523,12 @@ def roofline_extra(bound, achieved, tel, traffic):
 DEVICE = None  # ps_get_device_info of cuda:0, set in main
 
 
-def observe(run, seconds=1.5):
+def observe(run, seconds=None):
     """GPU clock and power while the leg's work repeats (after its timed region)."""
     import torch
+    seconds = TEL_SECONDS if seconds is None else seconds
+    if TEL_SECONDS <= 0 or seconds <= 0:
+        return {"available": False, "reason": "telemetry windows disabled (--telemetry-seconds 0)"}
     return TEL.observe(run, torch.cuda.synchronize, seconds=seconds)
 
 
@@ -554,6 +558,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--no-model70b", action="store_true", help="skip the 80-layer 70B-shaped model")
+    ap.add_argument("--telemetry-seconds", type=float, default=1.5,
+                    help="length of each leg's clock-and-power window after its timed region (0: none)")
     ap.add_argument("--phase-sweep", action="store_true",
                     help="also measure throughput, clock, power and energy per token across phases and batch sizes")
     ap.add_argument("--calib-copy", action="store_true",
@@ -574,9 +580,10 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
-    global TEL, DEVICE
+    global TEL, DEVICE, TEL_SECONDS
     from paper_2608_21719_amd.telemetry import Telemetry
     TEL = Telemetry(0)
+    TEL_SECONDS = a.telemetry_seconds
     DEVICE = B.device_info(0)
     if a.calib_copy:
         # int32 -> fp32 conversion copy: reads exactly 1 GiB, writes exactly 1 GiB
