@@ -504,6 +504,15 @@ ps_status ps_op_decode_plan(ps_kv* kv, int32_t n_seqs, const int32_t* seqs, int3
 ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
                            void* stream);
 
+/* ps_op_decode_run with the attention launch capped at max_workgroups
+ * workgroups (rounded down to a multiple of n_kv_heads, at least n_kv_heads):
+ * each workgroup then walks several split items in turn, the form the mixed
+ * step uses beside its prefill GEMMs. Same bits as the uncapped run (each
+ * item's arithmetic does not depend on which workgroup runs it).
+ * PS_E_INVALID for max_workgroups < 1; otherwise as ps_op_decode_run. */
+ps_status ps_op_decode_run_capped(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
+                                  int32_t max_workgroups, void* stream);
+
 /* Greedy token of each row of fp32 logits [rows, vocab] (ties -> lowest id). */
 ps_status ps_op_argmax(int32_t rows, int32_t vocab, const float* logits, int32_t* next, void* stream);
 

@@ -140,6 +140,7 @@ _SIGS = {
     "ps_op_decode_attention": (_I, [_P, _I, _I, _IP, _P, _P, _I, _P, c_size_t, _P]),
     "ps_op_decode_plan": (_I, [_P, _I, _IP, _I, _P, c_size_t, _P]),
     "ps_op_decode_run": (_I, [_P, _I, _P, _P, _P, c_size_t, _P]),
+    "ps_op_decode_run_capped": (_I, [_P, _I, _P, _P, _P, c_size_t, _I, _P]),
     "ps_op_argmax": (_I, [_I, _I, _P, _P, _P]),
     "ps_model_create": (_I, [POINTER(LayerCfg), _I, _I, _P, POINTER(LayerW), _P, _P, POINTER(c_void_p)]),
     "ps_model_destroy": (_I, [_P]),
@@ -549,3 +550,8 @@ def op_decode_plan(kv: KV, seqs, ws, split_pages=0, stream=None):
 def op_decode_run(kv: KV, layer, q, o, ws, stream=None):
     check(lib.ps_op_decode_run(kv.h, layer, ptr(q), ptr(o), ptr(ws), ws.numel() * ws.element_size(),
                                stream_handle(stream)))
+
+
+def op_decode_run_capped(kv: KV, layer, q, o, ws, max_workgroups, stream=None):
+    check(lib.ps_op_decode_run_capped(kv.h, layer, ptr(q), ptr(o), ptr(ws), ws.numel() * ws.element_size(),
+                                      max_workgroups, stream_handle(stream)))

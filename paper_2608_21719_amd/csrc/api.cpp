@@ -1557,9 +1557,9 @@ extern "C" ps_status ps_op_decode_plan(ps_kv* kv, int32_t n_seqs, const int32_t*
   PS_CATCH
 }
 
-extern "C" ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
-                                      void* stream) {
-  PS_TRY CHECK_KV(kv);
+static ps_status decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
+                            int32_t max_workgroups, void* stream) {
+  CHECK_KV(kv);
   if (ps_status rc = check_layer(kv, layer)) return rc;
   const DecodeAttnPlan& pl = kv->dplan;
   if (!pl.ws) return fail(PS_E_INVALID, "no decode attention plan on this handle");
@@ -1577,9 +1577,21 @@ extern "C" ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, v
                                (const SeqInfo*)(W + pl.o_si), (const int32_t*)(W + pl.o_bt),
                                (const DecodeItem*)(W + pl.o_di), (float*)(W + pl.off_po), (float*)(W + pl.off_pml),
                                (const int32_t*)(W + pl.o_pb), (const int32_t*)(W + pl.o_pc), o, scale_log2,
-                               (hipStream_t)stream);
+                               (hipStream_t)stream, max_workgroups);
   if (bad) return fail(PS_E_UNSUPPORTED, "decode attention configuration not supported");
   return last_launch_error();
+}
+
+extern "C" ps_status ps_op_decode_run(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  PS_TRY return decode_run(kv, layer, q, o, ws, ws_bytes, 0, stream);
+  PS_CATCH
+}
+
+extern "C" ps_status ps_op_decode_run_capped(ps_kv* kv, int32_t layer, const void* q, void* o, void* ws,
+                                             size_t ws_bytes, int32_t max_workgroups, void* stream) {
+  PS_TRY if (max_workgroups < 1) return fail(PS_E_INVALID, "max_workgroups must be at least 1");
+  return decode_run(kv, layer, q, o, ws, ws_bytes, max_workgroups, stream);
   PS_CATCH
 }
 

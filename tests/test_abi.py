@@ -229,6 +229,11 @@ def test_decode_run_needs_a_current_plan_and_its_workspace():
     assert B.lib.ps_op_decode_plan(kv.h, 0, None, -1, ws, nbytes, None) == B.PS_E_INVALID
     assert B.lib.ps_op_decode_run(kv.h, 0, None, None, ws, nbytes, None) == B.PS_E_INVALID  # failed plan leaves none
     assert "no decode attention plan" in B.last_error()
+    assert B.lib.ps_op_decode_plan(kv.h, 0, None, 0, ws, nbytes, None) == B.PS_OK
+    assert B.lib.ps_op_decode_run_capped(kv.h, 0, None, None, ws, nbytes, 0, None) == B.PS_E_INVALID
+    assert "max_workgroups" in B.last_error()
+    assert B.lib.ps_op_decode_run_capped(kv.h, 0, None, None, ws, nbytes, 1, None) == B.PS_OK
+    assert B.lib.ps_op_decode_run_capped(kv.h, 0, None, None, ws2, nbytes, 1, None) == B.PS_E_INVALID
 
 
 def test_unaligned_device_pointers_are_rejected_before_launch():

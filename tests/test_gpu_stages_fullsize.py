@@ -130,6 +130,13 @@ def test_decode_attention_at_the_benchmarked_split_plan(case):
         kf, vf = hist[b]
         ref = O.attention(qf[b:b + 1], kf, vf, np.array([ctx[b]]))[0]
         H.assert_close_elementwise(got[b], ref, H.BF16_TOL_ABS, H.BF16_TOL_REL, f"{case} b={b} ctx={ctx[b]}")
+    # the capped launch (the mixed step's form: fewer workgroups, each walking
+    # several split items) gives the same bits
+    for cap in (1, 8 * sh.n_kv, 128):
+        ocap = H.empty((nb, sh.d_q), "bf16")
+        B.op_decode_run_capped(kv, 0, q, ocap, aws, cap)
+        sync()
+        assert torch.equal(ocap.view(torch.int16), o.view(torch.int16)), f"{case}: capped at {cap} workgroups differs"
     gc = H.to_f64(oc).reshape(nb, sh.n_q, sh.head_dim)
     for b, c in enumerate(ctx):
         ref = _census_ref(c + 1, sh.n_kv, sh.head_dim, sh.group)
