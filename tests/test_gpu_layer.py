@@ -180,6 +180,62 @@ def test_8b_mixed_step_matches_oracle(h8):
         h.kv.free(s)
 
 
+def test_8b_forked_mixed_step_chunk_rows_equal_prefill_bit_for_bit(h8):
+    """The forked mixed step (more than 64 chunk rows beside decode rows: the
+    decode rows' attention, O, SwiGLU and down on the second stream, their
+    attention on a capped grid) against ps_prefill of the same chunks on a
+    second pool with the same history: the chunk rows take the same kernels
+    and plans either way, so their output and written K/V must match bit for
+    bit, whatever the decode rows do beside them on the other stream."""
+    h = h8
+    sh = h.shape
+    chunks = [(0, 150), (37, 96)]   # (cached prefix, chunk rows)
+    decs = [700, 1500, 90]          # decode rows' history lengths
+    hist = [p for p, _ in chunks] + decs
+    pools = [H.Pool(sh, sum((L + 160) // 16 for L in hist) + 8, 8, 128, seed=5 + i) for i in range(2)]
+    ws = [H.workspace(B.Layer.workspace_bytes(p.cfg, 512, 8, 128)) for p in pools]
+    g = torch.Generator(device="cuda").manual_seed(77)
+    kvh = [(torch.randn((L, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16),
+            torch.randn((L, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)) for L in hist]
+    seqs = []
+    for p, w in zip(pools, ws):
+        ss = []
+        for (pre, n), (k, v) in zip(chunks, kvh):
+            s = p.kv.open()
+            p.kv.alloc(s, pre + n)
+            if pre:
+                p.kv.append(0, [s], [pre], k, v, w)
+                p.kv.commit([s], [pre])
+            ss.append(s)
+        for L, (k, v) in zip(decs, kvh[len(chunks):]):
+            s = p.kv.open()
+            p.kv.alloc(s, L + 1)
+            p.kv.append(0, [s], [L], k, v, w)
+            p.kv.commit([s], [L])
+            ss.append(s)
+        seqs.append(ss)
+    n_chunk = sum(n for _, n in chunks)
+    xm = gen.mixed_input(h.wl, n_chunk + len(decs))
+    x = H.to_dev(xm, "bf16")
+    a, b = pools
+    out_m = H.empty((n_chunk + len(decs), sh.hidden), "bf16")
+    h.layer.mixed_step(h.dev.w, a.kv, 0, seqs[0][:2], [n for _, n in chunks], seqs[0][2:], x, out_m, ws[0])
+    out_p = H.empty((n_chunk, sh.hidden), "bf16")
+    h.layer.prefill(h.dev.w, b.kv, 0, seqs[1][:2], [n for _, n in chunks], x[:n_chunk].contiguous(), out_p, ws[1])
+    sync()
+    assert torch.equal(out_m[:n_chunk].view(torch.int16), out_p.view(torch.int16)), "chunk rows differ"
+    for (pre, n), sa, sb in zip(chunks, seqs[0][:2], seqs[1][:2]):
+        a.kv.commit([sa], [n])
+        b.kv.commit([sb], [n])
+        ka = torch.empty((pre + n, sh.n_kv, sh.head_dim), dtype=torch.bfloat16, device="cuda")
+        va, kb, vb = torch.empty_like(ka), torch.empty_like(ka), torch.empty_like(ka)
+        a.kv.gather(0, sa, ka, va, ws[0])
+        b.kv.gather(0, sb, kb, vb, ws[1])
+        sync()
+        assert torch.equal(ka.view(torch.int16), kb.view(torch.int16)), "written K differs"
+        assert torch.equal(va.view(torch.int16), vb.view(torch.int16)), "written V differs"
+
+
 def test_layer_rejects_capacity_overrun_without_launching(h8):
     h = h8
     s = h.open(16)
