@@ -72,6 +72,43 @@ __global__ __launch_bounds__(256) void issue_mix(float* out, int iters) {
   out[(long)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
+// Workgroups of eight waves, one per CU: waves w and w + 4 share SIMD w % 4.
+// MODE 0: waves 0-3 run MFMAs, waves 4-7 nothing; 1: waves 0-3 nothing,
+// waves 4-7 vector FMA chains; 2: both, on different waves of one SIMD.
+template <int MODE>
+__global__ __launch_bounds__(512) void cross_wave(float* out, int iters) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool do_m = wave < 4 && MODE != 1, do_v = wave >= 4 && MODE != 0;
+  f32x16 acc[4];
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  bf16x8 a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(1e-3f * (float)(threadIdx.x + e));
+    b[e] = (__bf16)(2e-3f * (float)e);
+  }
+  float v0 = threadIdx.x * 1e-3f, v1 = v0 + 1.f, v2 = v0 + 2.f, v3 = v0 + 3.f;
+  for (int i = 0; i < iters; ++i) {
+    if (do_m) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+    }
+    if (do_v) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        v0 = fmaf(v0, 1.0001f, 0.5f);
+        v1 = fmaf(v1, 0.9999f, 0.25f);
+        v2 = fmaf(v2, 1.0002f, 0.125f);
+        v3 = fmaf(v3, 0.9998f, 0.0625f);
+      }
+    }
+  }
+  float s = v0 + v1 + v2 + v3;
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) s += acc[j][r];
+  out[(long)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
 static float time_ms(hipEvent_t e0, hipEvent_t e1) {
   float ms = 0.f;
   CHECK(hipEventElapsedTime(&ms, e0, e1));
@@ -140,6 +177,20 @@ int main() {
   std::printf("vector fp32 FMA only:                   %.3f ms\n", t_v);
   std::printf("both in every wave, VGPR accumulators:  %.3f ms  (sum of the two alone %.3f ms)\n", t_b, t_m + t_v);
   std::printf("both in every wave, AGPR accumulators:  %.3f ms\n", t_a);
+  // the same split over different waves of one SIMD (one 8-wave workgroup per CU)
+  auto run8 = [&](auto kern) {
+    for (int w = 0; w < 3; ++w) hipLaunchKernelGGL(kern, dim3(cus), dim3(512), 0, 0, out, iters);
+    CHECK(hipEventRecord(e0));
+    hipLaunchKernelGGL(kern, dim3(cus), dim3(512), 0, 0, out, iters);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    return (double)time_ms(e0, e1);
+  };
+  const double x_m = run8(cross_wave<0>), x_v = run8(cross_wave<1>), x_b = run8(cross_wave<2>);
+  CHECK(hipGetLastError());
+  std::printf("MFMA waves alone (one per SIMD):        %.3f ms\n", x_m);
+  std::printf("FMA waves alone (one per SIMD):         %.3f ms\n", x_v);
+  std::printf("both, on different waves of each SIMD:  %.3f ms  (sum of the two alone %.3f ms)\n", x_b, x_m + x_v);
   std::printf("best: hbm read %.0f GB/s, hbm copy %.0f GB/s\n", best_rd, best_cp);
   CHECK(hipFree(out));
   return 0;
