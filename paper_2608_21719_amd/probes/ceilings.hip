@@ -109,6 +109,45 @@ __global__ __launch_bounds__(512) void cross_wave(float* out, int iters) {
   out[(long)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
+// Eight waves per CU (two per SIMD), every wave running 4 MFMAs and 64 FMAs
+// (four chains) per iteration, enough to keep the vector ALU busy; the waves
+// 4-7 first run OFF extra FMAs, so the two waves of a SIMD start out of phase.
+template <int OFF>
+__global__ __launch_bounds__(512) void phase_mix(float* out, int iters) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  f32x16 acc[4];
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  bf16x8 a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(1e-3f * (float)(threadIdx.x + e));
+    b[e] = (__bf16)(2e-3f * (float)e);
+  }
+  float v0 = threadIdx.x * 1e-3f, v1 = v0 + 1.f, v2 = v0 + 2.f, v3 = v0 + 3.f;
+  if (wave >= 4)
+    for (int k = 0; k < OFF / 4; ++k) {
+      v0 = fmaf(v0, 1.0001f, 0.5f);
+      v1 = fmaf(v1, 0.9999f, 0.25f);
+      v2 = fmaf(v2, 1.0002f, 0.125f);
+      v3 = fmaf(v3, 0.9998f, 0.0625f);
+    }
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      v0 = fmaf(v0, 1.0001f, 0.5f);
+      v1 = fmaf(v1, 0.9999f, 0.25f);
+      v2 = fmaf(v2, 1.0002f, 0.125f);
+      v3 = fmaf(v3, 0.9998f, 0.0625f);
+    }
+  }
+  float s = v0 + v1 + v2 + v3;
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) s += acc[j][r];
+  out[(long)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
 static float time_ms(hipEvent_t e0, hipEvent_t e1) {
   float ms = 0.f;
   CHECK(hipEventElapsedTime(&ms, e0, e1));
@@ -191,6 +230,9 @@ int main() {
   std::printf("MFMA waves alone (one per SIMD):        %.3f ms\n", x_m);
   std::printf("FMA waves alone (one per SIMD):         %.3f ms\n", x_v);
   std::printf("both, on different waves of each SIMD:  %.3f ms  (sum of the two alone %.3f ms)\n", x_b, x_m + x_v);
+  const double p0 = run8(phase_mix<0>), p1 = run8(phase_mix<32>);
+  CHECK(hipGetLastError());
+  std::printf("both in every wave, 2 waves per SIMD:   %.3f ms in phase, %.3f ms half an iteration apart\n", p0, p1);
   std::printf("best: hbm read %.0f GB/s, hbm copy %.0f GB/s\n", best_rd, best_cp);
   CHECK(hipFree(out));
   return 0;
