@@ -45,8 +45,8 @@ namespace ps {
 
 namespace {
 constexpr int kHd = 128;
-constexpr int kFaKT = 32;  // keys per tile (two pages)
-constexpr int kFaQB = 1;   // 32-row query blocks per wave
+constexpr int KT = 32;   // keys per tile (two pages, one per pair of waves)
+constexpr int kQT = 32;  // query rows per workgroup tile (one 32-row block per wave)
 }  // namespace
 
 // One 16-byte pool->LDS fill per lane through a buffer resource: a wave
@@ -55,7 +55,6 @@ __device__ __forceinline__ void fa_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
 }
 
-template <int QB, int KT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
@@ -63,8 +62,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
                                                          const PrefillItem* __restrict__ items,
                                                          bf16_t* __restrict__ o, int n_kv, int G, float scale_log2) {
   constexpr int NT = 256;
-  constexpr int kQT = 32 * QB;
-  static_assert(KT == 32 && QB == 1, "two pages per key tile, one page per pair of waves");
   constexpr int NPG = 2;
   constexpr int kKB = kPageTokens * kHd;  // elements of a page's K block (its V^T block follows)
   // K tile: 32 rows of 256 B; row r holds key 16 (r >> 4) + swap23(r & 15) (bits 2
@@ -260,22 +257,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
   }
 }
 
-int fa_query_tile() { return 32 * kFaQB; }
-
-template <int QB>
-int launch_fa_prefill_qb(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
-                         const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st) {
-  if (n_items == 0) return 0;
-  if (G % 4 != 0) return -1;
-  dim3 grid(n_items, n_kv * (G / 4));
-  hipLaunchKernelGGL((fa_prefill_kernel<QB, kFaKT>), grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si,
-                     bt, items, (bf16_t*)o, n_kv, G, scale_log2);
-  return 0;
-}
+int fa_query_tile() { return kQT; }
 
 int launch_fa_prefill(int G, int n_items, int n_kv, const void* q, const void* pool_layer, const SeqInfo* si,
                       const int32_t* bt, const PrefillItem* items, void* o, float scale_log2, hipStream_t st) {
-  return launch_fa_prefill_qb<kFaQB>(G, n_items, n_kv, q, pool_layer, si, bt, items, o, scale_log2, st);
+  if (n_items == 0) return 0;
+  if (G % 4 != 0) return -1;
+  dim3 grid(n_items, n_kv * (G / 4));
+  hipLaunchKernelGGL(fa_prefill_kernel, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)pool_layer, si, bt,
+                     items, (bf16_t*)o, n_kv, G, scale_log2);
+  return 0;
 }
 
 }  // namespace ps
