@@ -566,7 +566,7 @@ def main():
                     help="run one 1 GiB device copy first (known bytes, to scale rocprof counters)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+        print("bench.py measures one GPU only: libps has no multi-GPU path (run with --gpus 1)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -73,7 +73,7 @@ typedef int32_t ps_status;
 #define PS_E_CAPACITY 3    /* write beyond a sequence's reserved capacity, or a
                               sequence would exceed max_pages_per_seq            */
 #define PS_E_HIP 4         /* a HIP runtime call or launch failed                 */
-#define PS_E_UNSUPPORTED 5 /* valid request this build does not implement         */
+#define PS_E_UNSUPPORTED 5 /* valid request the library does not implement        */
 
 #define PS_PAGE_TOKENS 16  /* tokens per KV page                                  */
 #define PS_GATE_UP_BLOCK 32 /* row-interleave granularity of w_gate_up            */

@@ -951,7 +951,7 @@ ps_status plan_layer(const ps_layer_cfg& c, const ps_kv* kv, int32_t phase, int3
   // every GEMM of the call must be supported before anything is enqueued
   if (P.rows > 0 && (gemm_check(c.dtype, 0, P.rows, dq + 2 * dkv, d) || gemm_check(c.dtype, 1, P.rows, d, dq) ||
                      gemm_check(c.dtype, 2, P.rows, 2 * c.ffn, d) || gemm_check(c.dtype, 1, P.rows, d, c.ffn)))
-    return fail(PS_E_UNSUPPORTED, "GEMM shape not supported by this build");
+    return fail(PS_E_UNSUPPORTED, "GEMM shape not supported by libps");
   P.o_si = P.mt.add(cs.si.data(), cs.si.size() * sizeof(SeqInfo));
   P.o_bt = P.mt.add(cs.bt.data(), cs.bt.size() * 4);
   const std::vector<double> fr = inv_freq(c);
@@ -1224,7 +1224,7 @@ ps_status run_model(ps_model* M, ps_kv* kv, int32_t phase, int32_t n_chunk, cons
   if (ps_status rc = check_aligned({logits_out})) return rc;
   const int32_t n_out = n_chunk + n_dec;
   if (gemm_check(PS_BF16, PS_EPI_STORE, n_out, M->vocab, c.hidden))
-    return fail(PS_E_UNSUPPORTED, "LM head shape not supported by this build");
+    return fail(PS_E_UNSUPPORTED, "LM head shape not supported by libps");
   // last row of every sequence feeds the LM head
   std::vector<int32_t> last(n_out);
   {
