@@ -1,6 +1,6 @@
 """fp64 CPU oracle — TEST INFRASTRUCTURE ONLY.
 
-This package is the checker, never part of the product path. Only the tests,
+This package is the reference the tests check against, never part of the product path. Only the tests,
 ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
 import it. It shares no code with the HIP library or its Python binding; the
 only thing both sides consume is the seeded input generator in ``synth``.
