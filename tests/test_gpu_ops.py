@@ -436,10 +436,11 @@ def test_prefill_attention_ones_v_and_paging_invariance():
     assert np.all(H.to_f64(outs[(5, True)]) == 1.0)
 
 
-def test_prefill_attention_long_prefix_crosses_the_page_window():
-    """A 33-row chunk after a 33000-token prefix: the key walk spans more than
-    2048 pages (32768 positions), so the kernel's LDS cache of page ids moves
-    to its next window mid-walk; a short second sequence shares the launch."""
+def test_prefill_attention_long_prefix_33000_tokens():
+    """A 33-row chunk after a 33000-token prefix: a key walk of more than 2000
+    pages (1030 key tiles, each page id a scalar load one tile ahead and each
+    page's K/V a DMA through its own buffer resource); a short second sequence
+    shares the launch."""
     hist, new = [33000, 0], [33, 40]
     P = make_pool(S8, 2100, 2, 2090, seed=21)
     seqs, Ks, Vs = fill_kv(P, hist, new, "bf16", 700)
