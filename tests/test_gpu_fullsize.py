@@ -253,3 +253,60 @@ def test_70b_ragged_decode_and_short_prefill(layer70b):
     sync()
     ref = O.layer_sequence(layer70b["wf"], sh, gen.widen(xp, "bf16"))["out"]
     normwise_ok(H.to_f64(outp), ref, "prefill 256", layer70b["tol"])
+
+
+def test_70b_forked_mixed_step(layer70b):
+    """A forked mixed step at the 70B shape (G = 8: two flash workgroups per KV
+    head, the capped decode attention over 8 KV heads): a 200-row chunk after
+    a 3000-token cached prefix beside four decode rows. The chunk rows and the
+    K/V they write equal ps_prefill of the same chunk on a second pool with
+    the same history, bit for bit; the decode rows and the chunk's first and
+    last rows match the oracle."""
+    wl = layer70b["wl"]
+    sh = wl.shape
+    pre, n = 3000, 200
+    decs = [4096, 2000, 17, 900]
+    hist_len = [pre] + decs
+    pools = [H.Pool(sh, sum((L + 216) // 16 for L in hist_len) + 8, 8, 260, seed=31 + i) for i in range(2)]
+    ws = [H.workspace(B.Layer.workspace_bytes(p.cfg, 256, 8, 260)) for p in pools]
+    layers = [B.Layer(p.cfg) for p in pools]
+    g = torch.Generator(device="cuda").manual_seed(2024)
+    kvh = [(torch.randn((L, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16),
+            torch.randn((L, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)) for L in hist_len]
+    seqs = []
+    for p, w in zip(pools, ws):
+        ss = []
+        for i, (L, (k, v)) in enumerate(zip(hist_len, kvh)):
+            s = p.kv.open()
+            p.kv.alloc(s, L + (n if i == 0 else 1))
+            p.kv.append(0, [s], [L], k, v, w)
+            p.kv.commit([s], [L])
+            ss.append(s)
+        seqs.append(ss)
+    xm = gen.mixed_input(wl, n + len(decs))
+    x = H.to_dev(xm, "bf16")
+    out_m = H.empty((n + len(decs), sh.hidden), "bf16")
+    layers[0].mixed_step(layer70b["dev"].w, pools[0].kv, 0, seqs[0][:1], [n], seqs[0][1:], x, out_m, ws[0])
+    out_p = H.empty((n, sh.hidden), "bf16")
+    layers[1].prefill(layer70b["dev"].w, pools[1].kv, 0, seqs[1][:1], [n], x[:n].contiguous(), out_p, ws[1])
+    sync()
+    assert torch.equal(out_m[:n].view(torch.int16), out_p.view(torch.int16)), "chunk rows differ from ps_prefill"
+    pools[0].kv.commit(seqs[0][:1], [n])
+    pools[1].kv.commit(seqs[1][:1], [n])
+    ka = torch.empty((pre + n, sh.n_kv, sh.head_dim), dtype=torch.bfloat16, device="cuda")
+    va, kb, vb = torch.empty_like(ka), torch.empty_like(ka), torch.empty_like(ka)
+    pools[0].kv.gather(0, seqs[0][0], ka, va, ws[0])
+    pools[1].kv.gather(0, seqs[1][0], kb, vb, ws[1])
+    sync()
+    assert torch.equal(ka.view(torch.int16), kb.view(torch.int16)), "written K differs"
+    assert torch.equal(va.view(torch.int16), vb.view(torch.int16)), "written V differs"
+    got = H.to_f64(out_m)
+    xf = gen.widen(xm, "bf16")
+    kf, vf = H.to_f64(kvh[0][0]), H.to_f64(kvh[0][1])
+    ref = O.layer_rows(layer70b["wf"], sh, xf[:n], [0, n - 1], kf, vf)
+    normwise_ok(got[0], ref[0], "chunk row 0", layer70b["tol"])
+    normwise_ok(got[n - 1], ref[1], f"chunk row {n - 1}", layer70b["tol"])
+    for b, L in enumerate(decs):
+        kd, vd = H.to_f64(kvh[1 + b][0]), H.to_f64(kvh[1 + b][1])
+        ref = O.layer_sequence(layer70b["wf"], sh, xf[n + b:n + b + 1], kd, vd)["out"][0]
+        normwise_ok(got[n + b], ref, f"decode row {b} ctx {L}", layer70b["tol"])
