@@ -180,6 +180,36 @@ def test_8b_mixed_step_matches_oracle(h8):
         h.kv.free(s)
 
 
+@pytest.mark.parametrize("n_chunk,n_dec", [(40, 3), (70, 65)])
+def test_8b_unforked_mixed_step_matches_oracle(n_chunk, n_dec):
+    """Mixed steps that do not fork: 40 chunk rows (every stage on the
+    caller's stream over all rows, decode-sized GEMMs), and more than 64
+    decode rows beside 70 chunk rows (tile GEMMs over all rows)."""
+    h = Harness(CONFIGS["llama8b_prefill"], n_pages=400, max_seqs=80, max_pages=16, max_rows=4096)
+    lens = [20 + i for i in range(n_dec)]
+    c = h.open(n_chunk)
+    decs = [h.open(L + 1) for L in lens]
+    xp = gen.prefill_input(h.wl, sum(lens), step=11 + n_dec)
+    xpf = gen.widen(xp, "bf16")
+    h.prefill(decs, lens, xp)
+    checked = (0, n_dec - 1)
+    r0 = 0
+    for i, (s, L) in enumerate(zip(decs, lens)):
+        if i in checked:
+            h.oracle(s, xpf[r0:r0 + L])
+        r0 += L
+    xm = gen.mixed_input(h.wl, n_chunk + n_dec, layer=n_dec)
+    xmf = gen.widen(xm, "bf16")
+    out = H.empty((n_chunk + n_dec, h.shape.hidden), "bf16")
+    h.layer.mixed_step(h.dev.w, h.kv, 0, [c], [n_chunk], decs, H.to_dev(xm, "bf16"), out, h.ws)
+    sync()
+    got = H.to_f64(out)
+    check(got[:n_chunk], h.oracle(c, xmf[:n_chunk]), "bf16", f"unforked chunk ({n_chunk} + {n_dec})")
+    for i in checked:
+        ref = h.oracle(decs[i], xmf[n_chunk + i:n_chunk + i + 1])
+        check(got[n_chunk + i:n_chunk + i + 1], ref, "bf16", f"unforked decode {i} ({n_chunk} + {n_dec})")
+
+
 def test_8b_forked_mixed_step_chunk_rows_equal_prefill_bit_for_bit(h8):
     """The forked mixed step (more than 64 chunk rows beside decode rows: the
     decode rows' attention, O, SwiGLU and down on the second stream, their
