@@ -27,14 +27,16 @@
 // swizzle rather than padding, and the K rows are stored in a permuted
 // order (below) that makes P come out in the pool's key order.
 //
-// The per-score vector work is kept minimal: the running max is taken on
-// raw scores and the scale folds into one FMA per exponent, the output is
-// rescaled only when a row's max outgrows the exponent base by 2^8, the
-// half-wave max and sum exchanges are v_permlane32_swap, and the row sum l
-// is one packed bf16 dot product (v_dot2, against ones) per pair of P
-// values, accumulated in fp32: the sum of exactly the bf16 P values the PV
-// product uses, so V == 1 gives 1 to fp32 rounding, exactly 1 after the
-// bf16 store.
+// The per-score vector work is kept minimal. The softmax is invariant to
+// the exponent base subtracted from a row's scores, so the base is not the
+// running max: it is set from the row's true max only on the first tile
+// and whenever this tile's row sum, computed anyway, shows the base stale
+// (a sum past 2^32), so steady-state tiles take no max at all. The scale
+// folds into one FMA per exponent; the row sum l is one packed bf16 dot
+// product (v_dot2, against ones) per pair of P values, accumulated in
+// fp32: the sum of exactly the bf16 P values the PV product uses, so
+// V == 1 gives 1 to fp32 rounding, exactly 1 after the bf16 store. The
+// half-wave max and sum exchanges are v_permlane32_swap.
 //
 // 32 KB of LDS and 150 registers per lane let three workgroups (three
 // waves per SIMD) share a CU.
@@ -152,7 +154,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float lsum = 0.f;
-  float m = -INFINITY;
+  float m = -INFINITY, mb = -INFINITY;  // row max behind the exponent base, and the base m scale
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   const bf16x2_t ones2 = {(__bf16)1.0f, (__bf16)1.0f};
   // lane-constant LDS byte offsets of the operand reads
@@ -185,31 +187,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
         if (key > qpos) sacc[r] = -INFINITY;
       }
     }
-    float mx = sacc[0];
+    // P = 2^(s scale - mb) against the row's current exponent base mb, and
+    // this lane's partial row sum of the bf16 P values. The sum doubles as
+    // the test of the base: past 2^32 (or NaN or infinity, as from the
+    // initial base of -inf) the tile takes the slow path, which takes the
+    // row's true max over the tile, rescales O and l to it and redoes the
+    // exponentials. While the base stands no max is taken at all.
+    uint32_t pk[8];
+    auto exps = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-    {  // the other half's max (lane l +- 32) without an LDS round trip
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    }
-    if (__any((mx - m) * scale_log2 > 8.f)) {
+      for (int i = 0; i < 8; ++i)
+        pk[i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[2 * i], scale_log2, -mb)),
+                         __builtin_amdgcn_exp2f(fmaf(sacc[2 * i + 1], scale_log2, -mb)));
+      float lt = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) lt = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[i]), ones2, lt, false);
+      return lt;
+    };
+    float lt = exps();
+    if (__any(!(lt <= 0x1p32f))) {
+      float mx = sacc[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+      {  // the other half's max (lane l +- 32) without an LDS round trip
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      }
+      // key 0 is visible to every query row, so after the first tile m is finite
       const float m_new = fmaxf(m, mx);
-      const float alpha = __builtin_amdgcn_exp2f((m - m_new) * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f((m - m_new) * scale_log2);  // 0 while m = -inf
 #pragma unroll
       for (int db = 0; db < 4; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
       lsum *= alpha;
       m = m_new;
+      mb = m * scale_log2;
+      lt = exps();
     }
-    const float mb = m * scale_log2;
-    uint32_t pk[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      pk[i] = pack_bf2(__builtin_amdgcn_exp2f(fmaf(sacc[2 * i], scale_log2, -mb)),
-                       __builtin_amdgcn_exp2f(fmaf(sacc[2 * i + 1], scale_log2, -mb)));
-#pragma unroll
-    for (int i = 0; i < 8; ++i) lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[i]), ones2, lsum, false);
+    lsum += lt;
 #pragma unroll
     for (int kk2 = 0; kk2 < NPG; ++kk2) {
       const bf16x8_t bp = __builtin_bit_cast(bf16x8_t, make_uint4(pk[4 * kk2], pk[4 * kk2 + 1], pk[4 * kk2 + 2], pk[4 * kk2 + 3]));
