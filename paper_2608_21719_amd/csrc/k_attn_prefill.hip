@@ -57,6 +57,16 @@ __device__ __forceinline__ void fa_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voffset, 0, 0, 0);
 }
 
+// Workgroup barrier that publishes this wave's pool->LDS fills and LDS
+// writes: it waits for them first (vmcnt(0) lgkmcnt(0)). The fence of
+// __syncthreads() alone does not order the fills, whose LDS writes are
+// counted on vmcnt; without the wait a wave may pass the barrier before
+// its fills land and another wave reads the stale slot.
+__device__ __forceinline__ void fa_barrier() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void fa_prefill_kernel(const bf16_t* __restrict__ q,
                                                          const bf16_t* __restrict__ pool,
                                                          const SeqInfo* __restrict__ si,
@@ -236,18 +246,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bp, oacc[db], 0, 0, 0);
       }
     }
-    __syncthreads();  // this wave's fills of the next tile landed; every wave is done with this tile
+    fa_barrier();  // this wave's fills of the next tile landed; every wave is done with this tile
     if (kt + 1 < n_tiles && k0 + 2 * KT > kv_valid) {
       zero_tail(k0 + KT, nV);
-      __syncthreads();
+      fa_barrier();
     }
   };
 
   issue(0, page_id(0), sK0, sV0);
-  __syncthreads();
+  fa_barrier();
   if (KT > kv_valid) {
     zero_tail(0, sV0);
-    __syncthreads();
+    fa_barrier();
   }
   for (int kt = 0; kt < n_tiles; kt += 2) {
     tile(kt, sK0, sV0, sK1, sV1);
