@@ -128,7 +128,9 @@ def bench_prefill(torch, B, A, wl, steps, warmup):
     qa = randn(torch, gen, (tokens, sh.n_q, sh.head_dim))
     oa = torch.empty((tokens, sh.d_q), dtype=torch.bfloat16, device="cuda")
     attn_run = lambda: B.op_attention(kv, 0, seqs, [T] * n, qa, oa, ws)  # noqa: E731
-    a_ms = timer(attn_run, iters=max(5, steps))
+    # 0.3 ms launches: 100 untimed launches let the clock settle from the
+    # GEMM window above, then 200 are timed (about 0.1 s in all)
+    a_ms = timer(attn_run, iters=max(200, steps), warmup=100)
     tel_attn = observe(attn_run)
     traffic = measured_traffic("gate_up_gemm_8x2048", "paper_2608_21719_amd/csrc/k_gemm.hip")
     res = {

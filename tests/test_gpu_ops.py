@@ -421,6 +421,58 @@ def test_prefill_attention(shape):
         r0 += n
 
 
+@pytest.mark.parametrize("shape", [S8, S70], ids=["G4", "G8"])
+def test_prefill_attention_late_score_jumps(shape):
+    """Keys scaled by 8 to 48 in later key tiles lift some query rows' scores
+    tens to hundreds of log2 units above the exponent base the first tile
+    set, so P overflows the kernel's 2^32 row-sum check (or fp32 itself) and
+    the tile is redone against the new row max, several times per row and
+    in tiles that also hold ordinary keys. Random inputs only ever take that
+    path on the first tile."""
+    hist, new = [0, 300], [200, 65]
+    planted = {0: {70: 12.0, 140: 24.0, 199: 48.0}, 1: {200: 16.0, 330: 32.0, 364: 8.0}}
+    P = make_pool(shape, 200, 8, 40, seed=13)
+    kv = P.kv
+    seqs = [kv.open() for _ in hist]
+    ws = H.workspace(1 << 22)
+    Ks, Vs = [], []
+    for i, (sq, L, n) in enumerate(zip(seqs, hist, new)):
+        kv.alloc(sq, L + n)
+        k = gen.widen(rnd((L + n, shape.n_kv, shape.head_dim), "bf16", 900 + 2 * i), "bf16")
+        for key, a in planted[i].items():
+            k[key] *= a
+        k = gen.to_storage(k.astype(np.float32), "bf16")
+        v = rnd((L + n, shape.n_kv, shape.head_dim), "bf16", 901 + 2 * i)
+        Ks.append(k)
+        Vs.append(v)
+        if L:
+            kv.append(0, [sq], [L], H.to_dev(k[:L], "bf16"), H.to_dev(v[:L], "bf16"), ws)
+            kv.commit([sq], [L])
+        kv.append(0, [sq], [n], H.to_dev(k[L:], "bf16"), H.to_dev(v[L:], "bf16"), ws)
+    rows = sum(new)
+    q = rnd((rows, shape.n_q, shape.head_dim), "bf16", 62)
+    o = H.empty((rows, shape.d_q), "bf16")
+    B.op_attention(kv, 0, seqs, new, H.to_dev(q, "bf16"), o, ws)
+    sync()
+    got = H.to_f64(o).reshape(rows, shape.n_q, shape.head_dim)
+    assert np.all(np.isfinite(got))
+    qf = gen.widen(q, "bf16")
+    r0 = 0
+    for b, (L, n) in enumerate(zip(hist, new)):
+        ref = O.attention(qf[r0:r0 + n], gen.widen(Ks[b], "bf16"), gen.widen(Vs[b], "bf16"), np.arange(L, L + n))
+        H.assert_close_elementwise(got[r0:r0 + n], ref, H.BF16_TOL_ABS, H.BF16_TOL_REL, f"score jumps b={b}")
+        r0 += n
+    # the planted keys do move the base: rows of the first sequence whose max
+    # in later tiles exceeds the first tile's by more than 32 log2 units
+    G = shape.n_q // shape.n_kv
+    s0 = np.einsum("ihd,jhd->hij", qf[:new[0]], np.repeat(gen.widen(Ks[0], "bf16"), G, axis=1))
+    s0 = s0 * (np.log2(np.e) / np.sqrt(shape.head_dim))
+    causal = np.tril(np.ones((new[0], new[0]), bool))
+    s0 = np.where(causal, s0, -np.inf)
+    jumps = s0.max(axis=2) - s0[:, :, :32].max(axis=2)
+    assert np.count_nonzero(jumps > 32) > 100
+
+
 def test_prefill_attention_ones_v_and_paging_invariance():
     outs = {}
     for seed, ones in ((0, False), (999, False), (5, True)):
