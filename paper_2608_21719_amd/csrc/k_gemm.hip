@@ -315,8 +315,6 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   // column block). SwiGLU: the wave's column blocks alternate gate and up
   // (the 32-row interleave of w_gate_up), block 2p pairs with 2p + 1.
   constexpr int ROWF = 136;
-  lds_barrier_pinned();  // every wave is done reading operand slots
-  float* stg = (float*)smem + wave * (32 * ROWF);
   const int rbase = m0 + wm * WT, cbase = n0 + wn * WT;
   constexpr int V = std::is_same<TC, bf16_t>::value ? 8 : 4;  // columns per lane
   constexpr int OUT_COLS = EPI == 2 ? WT / 2 : WT;
@@ -329,21 +327,31 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
   using RRaw = typename std::conditional<std::is_same<TR, float>::value, float4,
                                          typename std::conditional<V == 8, uint4, uint2>::type>::type;
   constexpr int RCH = std::is_same<TR, float>::value ? V / 4 : 1;  // RRaw loads per pass
-#pragma unroll
-  for (int i = 0; i < Q; ++i) {
-    // residual loads of the whole 32-row block first: issued together, they
-    // overlap (R may alias C, so a load after a store would wait for it);
-    // each element is still read before it is written
-    RRaw rr[EPI == 1 ? NPASS : 1][RCH];
+  // Residual loads run one 32-row block ahead of the block being stored
+  // (two register sets), the first block's issued before the staging
+  // barrier, so that the HBM latency of the loads, which every CU issues at
+  // about the same moment, is exposed once per tile instead of once per
+  // block. Block i + 1's rows are disjoint from block i's, so the loads may
+  // precede block i's stores even where R aliases C, and every element is
+  // still read before it is written.
+  RRaw rr[2][EPI == 1 ? NPASS : 1][RCH];
+  auto load_r = [&](int i) __attribute__((always_inline)) {
     if constexpr (EPI == 1) {
 #pragma unroll
       for (int pass = 0; pass < NPASS; ++pass) {
         const int row = rbase + i * 32 + pass * RPP + lane / LPR, oc = (lane % LPR) * V;
         const long idx = (long)min(row, M - 1) * ldc + ccol + oc;  // rows past M: a valid row, result unused
 #pragma unroll
-        for (int q = 0; q < RCH; ++q) rr[pass][q] = *(const RRaw*)(R + idx + q * 4);
+        for (int q = 0; q < RCH; ++q) rr[i & 1][pass][q] = *(const RRaw*)(R + idx + q * 4);
       }
     }
+  };
+  load_r(0);
+  lds_barrier_pinned();  // every wave is done reading operand slots
+  float* stg = (float*)smem + wave * (32 * ROWF);
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    if (i + 1 < Q) load_r(i + 1);
 #pragma unroll
     for (int j = 0; j < Q; ++j)
 #pragma unroll
@@ -379,23 +387,23 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(const bf16_t* __restrict
         if constexpr (std::is_same<TR, float>::value) {
 #pragma unroll
           for (int q = 0; q < RCH; ++q) {
-            v[4 * q] += rr[pass][q].x;
-            v[4 * q + 1] += rr[pass][q].y;
-            v[4 * q + 2] += rr[pass][q].z;
-            v[4 * q + 3] += rr[pass][q].w;
+            v[4 * q] += rr[i & 1][pass][q].x;
+            v[4 * q + 1] += rr[i & 1][pass][q].y;
+            v[4 * q + 2] += rr[i & 1][pass][q].z;
+            v[4 * q + 3] += rr[i & 1][pass][q].w;
           }
         } else if constexpr (V == 8) {
-          const uint32_t w4[4] = {rr[pass][0].x, rr[pass][0].y, rr[pass][0].z, rr[pass][0].w};
+          const uint32_t w4[4] = {rr[i & 1][pass][0].x, rr[i & 1][pass][0].y, rr[i & 1][pass][0].z, rr[i & 1][pass][0].w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             v[2 * e] += bf_lo(w4[e]);
             v[2 * e + 1] += bf_hi(w4[e]);
           }
         } else {
-          v[0] += bf_lo(rr[pass][0].x);
-          v[1] += bf_hi(rr[pass][0].x);
-          v[2] += bf_lo(rr[pass][0].y);
-          v[3] += bf_hi(rr[pass][0].y);
+          v[0] += bf_lo(rr[i & 1][pass][0].x);
+          v[1] += bf_hi(rr[i & 1][pass][0].x);
+          v[2] += bf_lo(rr[i & 1][pass][0].y);
+          v[3] += bf_hi(rr[i & 1][pass][0].y);
         }
       }
       if (row >= M) continue;
