@@ -1,12 +1,18 @@
 // Attainable ceilings of one MI355X (gfx950), measured rather than taken
 // from the data sheet: HBM streaming read and copy bandwidth, the dense
-// bf16 MFMA rate of v_mfma_f32_32x32x16_bf16 on register operands, and
+// bf16 MFMA rate of v_mfma_f32_32x32x16_bf16 on register operands (near
+// constant, and random bits changing every product, as a GEMM on real data
+// sees; also v_mfma_f32_16x16x32_bf16 on the same random data), and
 // whether MFMA and vector-ALU work issued on the same SIMD overlap in time.
+// `ceilings mfma-random [seconds [32x32x16|16x16x32]]` runs only the
+// random-operand rates (or one of them) for about as long as asked, so that
+// clock and power can be sampled beside it.
 // A standalone program (not part of libps); every buffer is allocated here
 // and every kernel indexes inside it.
 #include <hip/hip_runtime.h>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 #include <vector>
 
 #define CHECK(x)                                                                 \
@@ -21,6 +27,64 @@
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Random bf16 operands that change from one product to the next: each wave
+// holds 4 A and 4 B fragments of random sign and mantissa bits (exponent
+// 126 or 127, so every value is normal and no sum overflows) and pairs
+// A j with B (j + r) % 4 in rotation r. SHAPE 0: 16 v_mfma_f32_32x32x16_bf16
+// per trip over 4 accumulators; SHAPE 1: 32 v_mfma_f32_16x16x32_bf16 (the
+// same FLOPs) over 16, each reused every 16 products. One trip is 524288
+// FLOP per wave.
+template <int SHAPE>
+__global__ __launch_bounds__(256) void mfma_random(float* out, int trips) {
+  unsigned h = (blockIdx.x * 256u + threadIdx.x) * 0x9E3779B9u + 0x7F4A7C15u;
+  auto next = [&]() {
+    h ^= h << 13;
+    h ^= h >> 17;
+    h ^= h << 5;
+    return h;
+  };
+  auto rnd_bf16 = [&]() {
+    const unsigned x = next();
+    const unsigned short bits = (unsigned short)((x & 0x807Fu) | ((x >> 8) & 1u ? 0x3F80u : 0x3F00u));
+    return __builtin_bit_cast(__bf16, bits);
+  };
+  bf16x8 a[4], b[4];
+  for (int j = 0; j < 4; ++j)
+    for (int e = 0; e < 8; ++e) {
+      a[j][e] = rnd_bf16();
+      b[j][e] = rnd_bf16();
+    }
+  float s = 0.f;
+  if constexpr (SHAPE == 0) {
+    f32x16 acc[4];
+    for (int j = 0; j < 4; ++j)
+      for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+    for (int t = 0; t < trips; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j], b[(j + r) & 3], acc[j], 0, 0, 0);
+    }
+    for (int j = 0; j < 4; ++j)
+      for (int r = 0; r < 16; ++r) s += acc[j][r];
+  } else {
+    f32x4 acc[16];
+    for (int j = 0; j < 16; ++j)
+      for (int r = 0; r < 4; ++r) acc[j][r] = 0.f;
+    for (int t = 0; t < trips; ++t) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j & 3], b[((j >> 2) + r) & 3], acc[j], 0, 0, 0);
+    }
+    for (int j = 0; j < 16; ++j)
+      for (int r = 0; r < 4; ++r) s += acc[j][r];
+  }
+  out[blockIdx.x * 256 + threadIdx.x] = s;
+}
 
 // grid-stride non-temporal 16-byte reads, folded so the loads stay live
 __global__ void hbm_read(const u32x4* __restrict__ p, long n, unsigned* out) {
@@ -154,13 +218,55 @@ static float time_ms(hipEvent_t e0, hipEvent_t e1) {
   return ms;
 }
 
-int main() {
+// bf16 MFMA rate on random operands, one 4-wave workgroup per CU (one wave
+// per SIMD, as the tile GEMM runs), each shape timed over about `seconds`
+static void mfma_random_rates(int cus, double seconds, hipEvent_t e0, hipEvent_t e1, int only_shape = -1) {
+  float* out = nullptr;
+  CHECK(hipMalloc(&out, (size_t)cus * 256 * sizeof(float)));
+  for (int shape = 0; shape < 2; ++shape) {
+    if (only_shape >= 0 && shape != only_shape) continue;
+    auto launch = [&](int trips) {
+      if (shape == 0) hipLaunchKernelGGL(mfma_random<0>, dim3(cus), dim3(256), 0, 0, out, trips);
+      else hipLaunchKernelGGL(mfma_random<1>, dim3(cus), dim3(256), 0, 0, out, trips);
+    };
+    // size a launch to about 50 ms from a short one, then repeat it
+    const int probe_trips = 20000;
+    launch(probe_trips);
+    CHECK(hipEventRecord(e0));
+    launch(probe_trips);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    float ms0 = 0.f;
+    CHECK(hipEventElapsedTime(&ms0, e0, e1));
+    const int trips = (int)(probe_trips * 50.0 / (ms0 > 0.01f ? ms0 : 0.01f));
+    const int reps = (int)(seconds * 1000.0 / 50.0) + 1;
+    CHECK(hipEventRecord(e0));
+    for (int r = 0; r < reps; ++r) launch(trips);
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    CHECK(hipGetLastError());
+    float ms = 0.f;
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+    const double flop = (double)cus * 4 * (double)trips * reps * 524288.0;
+    std::printf("mfma %s bf16, random operands changing every product: %.0f TFLOP/s (%.0f ms)\n",
+                shape == 0 ? "32x32x16" : "16x16x32", flop / (ms * 1e-3) / 1e12, ms);
+    std::fflush(stdout);
+  }
+  CHECK(hipFree(out));
+}
+
+int main(int argc, char** argv) {
   int dev = 0, cus = 0;
   CHECK(hipGetDevice(&dev));
   CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
+  if (argc > 1 && std::strcmp(argv[1], "mfma-random") == 0) {
+    const int only = argc > 3 ? (std::strcmp(argv[3], "16x16x32") == 0 ? 1 : 0) : -1;
+    mfma_random_rates(cus, argc > 2 ? std::atof(argv[2]) : 1.0, e0, e1, only);
+    return 0;
+  }
 
   // ---- HBM: 4 GiB source, far beyond the caches
   const long bytes = 4L << 30, n = bytes / 16;
@@ -234,6 +340,7 @@ int main() {
   CHECK(hipGetLastError());
   std::printf("both in every wave, 2 waves per SIMD:   %.3f ms in phase, %.3f ms half an iteration apart\n", p0, p1);
   std::printf("best: hbm read %.0f GB/s, hbm copy %.0f GB/s\n", best_rd, best_cp);
+  mfma_random_rates(cus, 1.0, e0, e1);
   CHECK(hipFree(out));
   return 0;
 }

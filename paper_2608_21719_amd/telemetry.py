@@ -17,6 +17,10 @@ Use:
                                       # enough for the driver's refresh rate
 When amdsmi is missing or refuses (no driver access), every result is
 {"available": False, "reason": ...} and measurements proceed without it.
+
+From the command line, `python -m paper_2608_21719_amd.telemetry -- CMD ...`
+runs CMD as a child process (GPU 0) and prints its output followed by the
+clock and power sampled while it ran, as one JSON line.
 """
 import threading
 import time
@@ -168,3 +172,29 @@ class Telemetry:
                     run()
                 sync()
         return rec.result
+
+
+def main(argv=None) -> int:
+    """Run a command as a child process and report GPU 0's clock and power
+    over its run (the child owns its own GPU work; nothing is exec'd)."""
+    import json
+    import subprocess
+    import sys
+    args = list(sys.argv[1:] if argv is None else argv)
+    if args and args[0] == "--":
+        args = args[1:]
+    if not args:
+        print("usage: python -m paper_2608_21719_amd.telemetry -- CMD [ARGS...]", file=sys.stderr)
+        return 2
+    tel = Telemetry(0)
+    with tel.leg() as rec:
+        r = subprocess.run(args, capture_output=True, text=True)
+    sys.stdout.write(r.stdout)
+    sys.stderr.write(r.stderr)
+    print(json.dumps({"command": args, "returncode": r.returncode, "static": tel.static_info(),
+                      "telemetry": rec.result}))
+    return r.returncode
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())
