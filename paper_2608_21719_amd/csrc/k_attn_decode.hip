@@ -239,11 +239,40 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(const float* __rest
   const int b = blockIdx.x, head = blockIdx.y, dim = threadIdx.x;
   const int kvh = head / G, hg = head - kvh * G;
   const int p0 = part_begin[b], np = part_count[b];
+  const long stride = (long)n_kv * G;  // between consecutive splits of one (sequence, head)
+  const long pi0 = ((long)p0 * n_kv + kvh) * G + hg;
+  // Loads go four splits at a time so that their latencies overlap; the
+  // arithmetic is the same sequence in split order as one split at a time.
   float M = -INFINITY;
-  for (int i = 0; i < np; ++i) M = fmaxf(M, part_ml[((((long)p0 + i) * n_kv + kvh) * G + hg) * 2]);
+  int i = 0;
+  for (; i + 4 <= np; i += 4) {
+    float mm[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) mm[u] = part_ml[(pi0 + (i + u) * stride) * 2];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) M = fmaxf(M, mm[u]);
+  }
+  for (; i < np; ++i) M = fmaxf(M, part_ml[(pi0 + i * stride) * 2]);
   float acc = 0.f, L = 0.f;
-  for (int i = 0; i < np; ++i) {
-    const long pi = (((long)p0 + i) * n_kv + kvh) * G + hg;
+  i = 0;
+  for (; i + 4 <= np; i += 4) {
+    float ov[4], mv[4], lv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const long pi = pi0 + (i + u) * stride;
+      ov[u] = part_o[pi * kHd + dim];
+      mv[u] = part_ml[pi * 2];
+      lv[u] = part_ml[pi * 2 + 1];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float f = exp2f(mv[u] - M);
+      acc += ov[u] * f;
+      L += lv[u] * f;
+    }
+  }
+  for (; i < np; ++i) {
+    const long pi = pi0 + i * stride;
     const float f = exp2f(part_ml[pi * 2] - M);
     acc += part_o[pi * kHd + dim] * f;
     L += part_ml[pi * 2 + 1] * f;
