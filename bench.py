@@ -538,6 +538,41 @@ def roofline_extra(bound, achieved, tel, traffic):
     return ex
 
 
+def mfma_random_ceiling(seconds=1.0):
+    """The matrix cores' rate on random bf16 operands that change every
+    product, as a GEMM on N(0, s) data sees (the ceilings probe, run as a
+    child process on this GPU, with the clock and power sampled beside it):
+    the data sheet's 2.5 PFLOP/s assumes a clock that such data does not
+    hold. None when the probe is not built."""
+    import re
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2608_21719_amd", "probes", "ceilings")
+    if not os.path.exists(exe):
+        return None
+    try:
+        if TEL is not None and TEL.available:
+            with TEL.leg() as rec:
+                r = subprocess.run([exe, "mfma-random", str(seconds), "32x32x16"], capture_output=True, text=True,
+                                   timeout=60)
+            tel = rec.result
+        else:
+            r = subprocess.run([exe, "mfma-random", str(seconds), "32x32x16"], capture_output=True, text=True,
+                               timeout=60)
+            tel = None
+    except (OSError, subprocess.TimeoutExpired) as e:
+        return {"error": f"{type(e).__name__}: {e}"}
+    m = re.search(r"random operands changing every product: (\d+) TFLOP/s", r.stdout)
+    if r.returncode != 0 or not m:
+        return {"error": f"probe exit {r.returncode}: {r.stderr.strip()[-200:]}"}
+    out = {"tflops": float(m.group(1)), "source": "paper_2608_21719_amd/probes/ceilings mfma-random (v_mfma_f32_32x32x16_bf16, "
+                                                   "one wave per SIMD, random sign and mantissa bits)"}
+    if tel and tel.get("gfxclk_mhz"):
+        out["gfxclk_mhz_median"] = tel["gfxclk_mhz"]["median"]
+    if tel and tel.get("power_w"):
+        out["power_w_median"] = tel["power_w"]["median"]
+    return out
+
+
 DEVICE = None  # ps_get_device_info of cuda:0, set in main
 
 
@@ -614,6 +649,10 @@ def main():
     dec_wl = CONFIGS["llama8b_decode"]
     log(f"prefill: {pre_wl.note}")
     pre = bench_prefill(torch, B, A, pre_wl, a.steps, a.warmup)
+    ceil = mfma_random_ceiling()
+    if ceil and "tflops" in ceil:
+        ceil["gate_up_frac"] = pre["roofline"]["achieved"] / ceil["tflops"]
+    pre["roofline"]["mfma_ceiling_random_operands"] = ceil
     log(f"prefill: {pre['tok_s']:.0f} tok/s, {pre['ms_per_step']:.3f} ms/step, gate_up {pre['gate_up_gemm']['tflops']:.0f} TFLOP/s")
     torch.cuda.empty_cache()
     dec = None
