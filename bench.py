@@ -538,12 +538,14 @@ def roofline_extra(bound, achieved, tel, traffic):
     return ex
 
 
-def mfma_random_ceiling(seconds=1.0):
+def mfma_random_ceiling(seconds=2.5):
     """The matrix cores' rate on random bf16 operands that change every
     product, as a GEMM on N(0, s) data sees (the ceilings probe, run as a
     child process on this GPU, with the clock and power sampled beside it):
     the data sheet's 2.5 PFLOP/s assumes a clock that such data does not
-    hold. None when the probe is not built."""
+    hold. None when the probe is not built. The window is long enough
+    that the sampled medians fall in the busy part, not the child's
+    start-up."""
     import re
     import subprocess
     exe = os.path.join(ROOT, "paper_2608_21719_amd", "probes", "ceilings")
