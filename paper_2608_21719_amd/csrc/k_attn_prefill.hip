@@ -43,6 +43,8 @@
 #include "common.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace ps {
 
 namespace {
@@ -164,7 +166,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float lsum = 0.f;
-  float m = -INFINITY, mb = -INFINITY;  // row max behind the exponent base, and the base m scale
+  float m = -INFINITY, mb = -INFINITY;  // row max behind the exponent base (set by the first tile), and m scale
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   const bf16x2_t ones2 = {(__bf16)1.0f, (__bf16)1.0f};
   // lane-constant LDS byte offsets of the operand reads
@@ -173,7 +175,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
 
   // one key tile: K, V hold it; the next tile's fills go to nK, nV
   int pid_next = n_tiles > 1 ? page_id(KT) : 0;
-  auto tile = [&](int kt, const bf16_t* K, const bf16_t* V, bf16_t* nK, bf16_t* nV) {
+  // `firstc`: std::true_type for the walk's first tile, which sets the base
+  auto tile = [&](int kt, const bf16_t* K, const bf16_t* V, bf16_t* nK, bf16_t* nV, auto firstc) {
+    constexpr bool FIRST = decltype(firstc)::value;
     const int k0 = kt * KT;
     if (kt + 1 < n_tiles) {
       issue(k0 + KT, pid_next, nK, nV);
@@ -197,12 +201,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
         if (key > qpos) sacc[r] = -INFINITY;
       }
     }
-    // P = 2^(s scale - mb) against the row's current exponent base mb, and
-    // this lane's partial row sum of the bf16 P values. The sum doubles as
-    // the test of the base: past 2^32 (or NaN or infinity, as from the
-    // initial base of -inf) the tile takes the slow path, which takes the
-    // row's true max over the tile, rescales O and l to it and redoes the
-    // exponentials. While the base stands no max is taken at all.
+    // P = 2^(s scale - mb) against the row's exponent base mb, and this
+    // lane's partial row sum of the bf16 P values. The first tile sets the
+    // base from its own row max (key 0 is visible to every query row, so that
+    // max is finite). After it, the sum doubles as the test of the base: past
+    // 2^32 (or infinite or NaN, where an exponent overflowed) the tile takes
+    // the slow path, which takes the row's true max over the tile, rescales O
+    // and l to it and redoes the exponentials. While the base stands no max
+    // is taken at all.
     uint32_t pk[8];
     auto exps = [&]() __attribute__((always_inline)) {
 #pragma unroll
@@ -214,26 +220,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
       for (int i = 0; i < 8; ++i) lt = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[i]), ones2, lt, false);
       return lt;
     };
-    float lt = exps();
-    if (__any(!(lt <= 0x1p32f))) {
+    auto row_max = [&]() __attribute__((always_inline)) {
       float mx = sacc[0];
 #pragma unroll
       for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-      {  // the other half's max (lane l +- 32) without an LDS round trip
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-      }
-      // key 0 is visible to every query row, so after the first tile m is finite
-      const float m_new = fmaxf(m, mx);
-      const float alpha = __builtin_amdgcn_exp2f((m - m_new) * scale_log2);  // 0 while m = -inf
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      lsum *= alpha;
-      m = m_new;
+      // the other half's max (lane l +- 32) without an LDS round trip
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    };
+    float lt;
+    if constexpr (FIRST) {
+      m = row_max();
       mb = m * scale_log2;
       lt = exps();
+    } else {
+      lt = exps();
+      if (__any(!(lt <= 0x1p32f))) {
+        const float m_new = fmaxf(m, row_max());
+        const float alpha = __builtin_amdgcn_exp2f((m - m_new) * scale_log2);
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+        lsum *= alpha;
+        m = m_new;
+        mb = m * scale_log2;
+        lt = exps();
+      }
     }
     lsum += lt;
 #pragma unroll
@@ -259,9 +272,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
     zero_tail(0, sV0);
     fa_barrier();
   }
-  for (int kt = 0; kt < n_tiles; kt += 2) {
-    tile(kt, sK0, sV0, sK1, sV1);
-    if (kt + 1 < n_tiles) tile(kt + 1, sK1, sV1, sK0, sV0);
+  // tile t sits in slot t & 1; the first tile is peeled (it sets the base)
+  tile(0, sK0, sV0, sK1, sV1, std::true_type{});
+  for (int kt = 1; kt < n_tiles; kt += 2) {
+    tile(kt, sK1, sV1, sK0, sV0, std::false_type{});
+    if (kt + 1 < n_tiles) tile(kt + 1, sK0, sV0, sK1, sV1, std::false_type{});
   }
 
   {
