@@ -166,6 +166,55 @@ def test_decode_batch64_sampled_sequences(layer8b):
     assert min(ctx) >= 1024 and max(ctx) <= 4096
 
 
+def test_decode_batch64_four_steps_sampled_sequences(layer8b):
+    """Four consecutive decode steps of the B = 64 benchmark batch (fresh
+    inputs each step): every step writes its token's K/V and the next step
+    reads it back. Sampled sequences include one whose length crosses a
+    16-token page boundary during the four steps; each step's rows are
+    compared with the oracle's layer over the history plus the steps so far
+    (one sequence, causal)."""
+    wl = CONFIGS["llama8b_decode"]
+    sh = wl.shape
+    steps = 4
+    ctx = [int(c) for c in gen.context_lengths(wl)]
+    nb = len(ctx)
+    crossing = next(b for b, c in enumerate(ctx) if c % 16 >= 16 - steps + 1)
+    sample = sorted({0, crossing, nb - 1})
+    max_pages = (max(ctx) + steps + 15) // 16
+    n_pages = sum((c + steps + 15) // 16 for c in ctx) + 8
+    pool = H.Pool(sh, n_pages, nb, max_pages, seed=gen.page_order_seed(wl))
+    kv = pool.kv
+    layer = B.Layer(pool.cfg)
+    ws = H.workspace(B.Layer.workspace_bytes(pool.cfg, 64, nb, max_pages))
+    g = torch.Generator(device="cuda").manual_seed(wl.cfg_id * 1000 + 11)
+    seqs = [kv.open() for _ in range(nb)]
+    hist = {}
+    for b, (sq, c) in enumerate(zip(seqs, ctx)):
+        kv.alloc(sq, c + steps)
+        k = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((c, sh.n_kv, sh.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        kv.append(0, [sq], [c], k, v, ws)
+        kv.commit([sq], [c])
+        if b in sample:
+            hist[b] = (H.to_f64(k), H.to_f64(v))
+        del k, v
+    xs, outs = [], []
+    for t in range(steps):
+        x = gen.decode_input(wl, nb, t)
+        out = H.empty((nb, sh.hidden), "bf16")
+        layer.decode_step(layer8b["dev"].w, kv, 0, B.PS_PHASE_ANSWER, seqs, H.to_dev(x, "bf16"), out, ws)
+        kv.commit(seqs, [1] * nb)
+        xs.append(gen.widen(x, "bf16"))
+        outs.append(out)
+    sync()
+    assert [kv.seq_len(sq) for sq in seqs] == [c + steps for c in ctx]
+    for b in sample:
+        rows = np.stack([xs[t][b] for t in range(steps)])
+        ref = O.layer_sequence(layer8b["wf"], sh, rows, *hist[b])["out"]
+        for t in range(steps):
+            normwise_ok(H.to_f64(outs[t])[b], ref[t], f"decode seq {b} ctx {ctx[b]} step {t}")
+
+
 def test_think_batch32_long_context_sampled_sequences(layer8b):
     wl = CONFIGS["llama8b_think"]
     ctx = [int(c) for c in gen.context_lengths(wl)]
