@@ -495,23 +495,39 @@ int32_t choose_split_pages(const std::vector<SeqInfo>& si, size_t first, int n_k
   (void)phase;
   long total = 0;
   for (size_t b = first; b < si.size(); ++b) total += (si[b].kv_before + si[b].n_new + 15) / 16;
-  // about 1024 workgroups over the chip (two rounds of the 512 that fit at
-  // two per CU), at least 8 pages per split. Measured over split sizes on
-  // the 8B decode and think and the 70B decode workloads: every workgroup
-  // pays a ramp-up (its first pages' latency) and a merge, so fewer, longer
-  // splits stream faster down to ~1000 workgroups (3072: 5-10% slower).
-  const long target_items = std::max(1, 1024 / std::max(1, n_kv));
-  long sp = (total + target_items - 1) / target_items;
-  sp = std::max<long>(sp, 8);
-  sp = (sp + 3) / 4 * 4;
-  // the work-item index is a grid y coordinate (at most 65535): widen the
-  // splits until the items fit (a batch of more sequences than that is
-  // rejected by the launcher)
+  // At most about 1024 workgroups over the chip: two full rounds of the 512
+  // that fit at two per CU, at least 8 pages per split, a multiple of 4 (the
+  // four waves of a workgroup walk pages w, w + 4, ...). Measured over split
+  // sizes on the 8B decode and think and the 70B decode workloads: every
+  // workgroup pays a ramp-up (its first pages' latency) and a merge, so
+  // fewer, longer splits stream faster down to ~1000 workgroups (3072: 5-10%
+  // slower), and a plan that spills a few items into a third round pays for
+  // that round (think batch: 1152 workgroups 285 us, 1000 workgroups 274 us).
+  // So the split is the smallest that keeps the grid within two rounds,
+  // where one exists; a batch of more sequences than two rounds hold gets
+  // one split per sequence.
   auto n_items = [&](long spl) {
     long n = 0;
     for (size_t b = first; b < si.size(); ++b) n += ((si[b].kv_before + si[b].n_new + 15) / 16 + spl - 1) / spl;
     return n;
   };
+  long max_pages = 8;
+  for (size_t b = first; b < si.size(); ++b) max_pages = std::max<long>(max_pages, (si[b].kv_before + si[b].n_new + 15) / 16);
+  const long target_items = std::max(1, 1024 / std::max(1, n_kv));
+  long sp = std::max<long>((total + target_items - 1) / target_items, 8);
+  sp = (sp + 3) / 4 * 4;
+  if (n_items(sp) > target_items) {  // smallest multiple of 4 in (sp, max_pages] that fits: n_items falls as sp grows
+    long lo = sp / 4, hi = (max_pages + 3) / 4;
+    while (lo + 1 < hi) {
+      const long mid = (lo + hi) / 2;
+      if (n_items(4 * mid) <= target_items) hi = mid;
+      else lo = mid;
+    }
+    sp = 4 * hi;
+  }
+  // the work-item index is a grid y coordinate (at most 65535): widen the
+  // splits until the items fit (a batch of more sequences than that is
+  // rejected by the launcher)
   while (n_items(sp) > kMaxDecodeItems && sp < (1L << 24)) sp *= 2;
   return (int32_t)sp;
 }
