@@ -480,8 +480,11 @@ ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_
  * (the row's own K/V already written there, not yet committed), attending
  * over keys 0..len. q [n_seqs, n_q, hd], o [n_seqs, n_q * hd].
  * split_pages = at most that many pages per split: each sequence's pages
- * are cut into ceil(pages / split_pages) splits of near-equal size (0 =
- * library choice). PS_E_UNSUPPORTED when the splits come to more than 65535
+ * are cut into ceil(pages / split_pages) splits of near-equal size. 0 =
+ * library choice: the smallest multiple of 4 pages, at least 8, that keeps
+ * the work items (splits times KV heads) within about 1024 workgroups, two
+ * full rounds of the chip; one split per sequence when the batch alone
+ * exceeds that. PS_E_UNSUPPORTED when the splits come to more than 65535
  * work items (one grid row each). */
 ps_status ps_op_decode_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_t* seqs,
                                  const void* q, void* o, int32_t split_pages, void* ws, size_t ws_bytes,
