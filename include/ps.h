@@ -482,7 +482,7 @@ ps_status ps_op_attention(ps_kv* kv, int32_t layer, int32_t n_seqs, const int32_
  * split_pages = at most that many pages per split: each sequence's pages
  * are cut into ceil(pages / split_pages) splits of near-equal size. 0 =
  * library choice: the smallest multiple of 4 pages, at least 8, that keeps
- * the work items (splits times KV heads) within about 1024 workgroups, two
+ * the workgroups (splits times KV heads) within about 1024, two
  * full rounds of the chip; one split per sequence when the batch alone
  * exceeds that. PS_E_UNSUPPORTED when the splits come to more than 65535
  * work items (one grid row each). */
