@@ -374,6 +374,44 @@ def test_decode_attention_ones_v_gives_exactly_one():
     assert np.all(H.to_f64(o) == 1.0)
 
 
+def library_split_pages(page_counts, n_kv):
+    """The library's documented split choice, restated: the smallest multiple
+    of 4 pages, at least 8, whose splits times KV heads stay within 1024
+    workgroups (one split per sequence when none does)."""
+    target = max(1, 1024 // max(1, n_kv))
+    n_items = lambda sp: sum(-(-p // sp) for p in page_counts)
+    sp = max(-(-sum(page_counts) // target), 8)
+    sp = -(-sp // 4) * 4
+    while n_items(sp) > target and sp < max(page_counts):
+        sp += 4
+    return sp
+
+
+@pytest.mark.parametrize("n_seqs,hist,expect", [(100, 130, 12), (16, 2000, 16)], ids=["search", "direct"])
+def test_decode_library_split_choice(n_seqs, hist, expect):
+    """split_pages = 0 gives the same bits as the split the documented rule
+    names, and other bits than a split 4 pages smaller (the split fixes the
+    merge's rounding order, so the comparison tells splits apart). 100
+    sequences of 9 pages: 8 pages per split would make 200 items for 128
+    slots, so the rule moves on to 12; 16 sequences of 126 pages: 16 directly."""
+    shape = S8
+    pages = [-(-(hist + 1) // 16)] * n_seqs
+    sp = library_split_pages(pages, shape.n_kv)
+    assert sp == expect
+    P = make_pool(shape, sum(pages) + 16, n_seqs, max(pages) + 2, seed=31)
+    seqs, _, _ = fill_kv(P, [hist] * n_seqs, [1] * n_seqs, "bf16", 300)
+    q = H.to_dev(rnd((n_seqs, shape.n_q, shape.head_dim), "bf16", 53), "bf16")
+    ws = H.workspace(1 << 26)
+    outs = {}
+    for split in (0, sp, sp - 4):
+        o = H.empty((n_seqs, shape.d_q), "bf16")
+        B.op_decode_attention(P.kv, 0, seqs, q, o, ws, split_pages=split)
+        sync()
+        outs[split] = H.bits(o)
+    np.testing.assert_array_equal(outs[0], outs[sp])
+    assert np.any(outs[sp - 4] != outs[sp])
+
+
 def test_decode_plan_run_matches_one_call_and_detects_pool_change():
     """Plan once, run for two layers: bit-identical to the one-call op; a
     commit invalidates the plan."""
